@@ -1,0 +1,116 @@
+// Device helpers shared by the fused, unfused and decode kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fqk {
+
+typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef __bf16 bf16x2_t __attribute__((__vector_size__(2 * sizeof(__bf16))));
+typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
+typedef uint32_t u32x4_t __attribute__((__vector_size__(4 * sizeof(uint32_t))));
+
+// ---------------------------------------------------------------------------
+// INT4 -> bf16 MFMA operand.
+//
+// A 32-bit word of Wq holds the codes of 8 consecutive k of one column, code
+// j in bits 4j..4j+3.  The bf16 value 16 + q has bit pattern 0x4180 | (q << 3)
+// (exponent 2^4, q in the top four mantissa bits), so a shift and an and-or
+// turn two codes into a packed bf16 pair without any conversion instruction.
+// The pairs come out as (k0,k4), (k1,k5), (k2,k6), (k3,k7); the activation
+// operand is staged in LDS in that same order, so the 8-term dot product the
+// MFMA forms per lane is unchanged.  The offset 16 + z is removed after each
+// 128-row group with the exact identity
+//     sum_k x_k (q_k - z) = sum_k x_k (16 + q_k) - (16 + z) sum_k x_k,
+// so (q - z) never needs to be formed and the scale s is applied in fp32 once
+// per group (eq. 3 of the paper).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bf16x8_t dequant_word(uint32_t w) {
+  const uint32_t mask = 0x00780078u, bias = 0x41804180u;
+  u32x4_t r;
+  r[0] = ((w << 3) & mask) | bias;
+  r[1] = ((w >> 1) & mask) | bias;
+  r[2] = ((w >> 5) & mask) | bias;
+  r[3] = ((w >> 9) & mask) | bias;
+  return __builtin_bit_cast(bf16x8_t, r);
+}
+
+// Position of element k%8 inside an 8-element chunk of the LDS activation
+// rows: chunk order is (x0, x4, x1, x5, x2, x6, x3, x7).
+__device__ __forceinline__ uint32_t chunk_pos(uint32_t k) {
+  return (k & ~7u) | ((k & 3u) << 1) | ((k >> 2) & 1u);
+}
+
+// Same map applied to four packed u8 row indices at once.
+__device__ __forceinline__ uint32_t chunk_pos4(uint32_t k4) {
+  return (k4 & 0xF8F8F8F8u) | ((k4 & 0x03030303u) << 1) | ((k4 >> 2) & 0x01010101u);
+}
+
+// 16 bytes of X (x0..x7) -> chunk order (x0,x4,x1,x5,x2,x6,x3,x7).
+__device__ __forceinline__ uint4 permute_chunk(uint4 w) {
+  uint4 o;
+  o.x = (w.x & 0xFFFFu) | (w.z << 16);
+  o.y = (w.x >> 16) | (w.z & 0xFFFF0000u);
+  o.z = (w.y & 0xFFFFu) | (w.w << 16);
+  o.w = (w.y >> 16) | (w.w & 0xFFFF0000u);
+  return o;
+}
+
+// ---------------------------------------------------------------------------
+// One Tile-COO group (16 bytes, four slots), decoded as the paper's outlier
+// decoding step describes (Sec. 4.2): four u8 rows, four u8 columns, four
+// bf16 values; value bits 0x0000 mark a padding slot.
+// ---------------------------------------------------------------------------
+struct Group {
+  uint32_t rows;   // k0 | k1 << 8 | k2 << 16 | k3 << 24 (tile-local)
+  uint32_t cols;   // n0 | n1 << 8 | n2 << 16 | n3 << 24 (tile-local)
+  uint32_t v01;    // bf16 v0 | v1 << 16
+  uint32_t v23;    // bf16 v2 | v3 << 16
+};
+
+__device__ __forceinline__ Group decode_group(uint4 g) {
+  Group d;
+  d.rows = g.x;
+  d.cols = g.y;
+  d.v01 = g.z;
+  d.v23 = g.w;
+  return d;
+}
+
+__device__ __forceinline__ uint32_t slot_row(const Group& d, int j) { return (d.rows >> (8 * j)) & 0xFFu; }
+__device__ __forceinline__ uint32_t slot_col(const Group& d, int j) { return (d.cols >> (8 * j)) & 0xFFu; }
+__device__ __forceinline__ uint32_t slot_val(const Group& d, int j) {
+  return ((j < 2 ? d.v01 : d.v23) >> (16 * (j & 1))) & 0xFFFFu;
+}
+// All four slots in one column (always true in by-column mode).
+__device__ __forceinline__ bool single_column(const Group& d) {
+  return d.cols == (d.cols & 0xFFu) * 0x01010101u;
+}
+
+// ---------------------------------------------------------------------------
+// Number formats.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits) {
+  return __builtin_bit_cast(float, bits << 16);
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint32_t bits) {
+  return float(__builtin_bit_cast(_Float16, uint16_t(bits)));
+}
+
+// fp32 -> bf16, round to nearest, ties to even (IEEE 754 rounding applied to
+// the 16 dropped bits); NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return ((u >> 16) | 0x40u) & 0xFFFFu;
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                         __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+}  // namespace fqk

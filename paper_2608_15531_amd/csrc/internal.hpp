@@ -1,0 +1,62 @@
+// Internal interface between the C ABI (capi.cpp) and the HIP launchers
+// (kernels.hip).  Not installed; not part of the public ABI.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fqi {
+
+constexpr int kTileK = 128;     // K side of a dense/sparse tile = quantisation group
+constexpr int kTileN = 64;      // N side of a tile = one output strip
+constexpr int kThreads = 256;   // four wave64 per workgroup
+constexpr int kMaxM = 32;       // rows the fused GEMV-regime kernel supports
+constexpr int kMaxBuckets = 256;
+
+// Launch plan of one matmul kernel.  Everything that sizes the workspace
+// depends only on (M, K, N, split_k) so the workspace can be sized before the
+// Tile-COO exists.
+struct Plan {
+  int M, K, N;
+  int MB;            // 16-row blocks: 1 (M <= 16) or 2 (M <= 32)
+  int n_strips;      // N / 64
+  int T;             // tiles per strip, K / 128
+  int S;             // K ranges per strip (split-K)
+  int nt_max;        // most tiles one workgroup covers
+  int xstride;       // LDS row stride of the staged activations, elements
+  int B;             // buckets per tile
+  int stage_cap;     // Tile-COO groups the LDS stage holds
+  // dynamic LDS layout, bytes
+  size_t off_xsum, off_shc, off_stage, off_binfo, off_tptr, off_flag, lds_bytes;
+  // workspace layout, bytes
+  size_t partial_bytes, counter_offset, ws_bytes;
+};
+
+// Returns false when (M, K, N) is outside what the kernels implement.
+bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
+               int64_t max_tile_groups, Plan* plan);
+
+struct MatmulPtrs {
+  const uint16_t* X;
+  const uint32_t* Wq;
+  const uint16_t* scales;
+  const uint32_t* zeros;
+  const uint32_t* tile_indptr;
+  const uint16_t* bucket_info;
+  const uint32_t* packed;
+  int64_t n_groups;
+  const float* y_addend;   // fp32 [M][N] added before the output is written, or null
+  void* Y;
+  int y_f32;
+  void* workspace;
+};
+
+// Enqueues one matmul kernel; returns a hipError_t value (0 on success).
+int launch_matmul(const Plan& plan, const MatmulPtrs& p, bool dense, bool sparse, void* stream);
+
+// Enqueues the group decoder over every group; returns a hipError_t value.
+int launch_decode(const uint32_t* tile_indptr, int64_t n_tiles, const uint32_t* packed,
+                  int64_t n_groups, int kt_count, int k_tile, int n_tile, int32_t* k_out,
+                  int32_t* n_out, uint16_t* v_out, void* stream);
+
+}  // namespace fqi

@@ -11,6 +11,7 @@ from .gen import (  # noqa: F401
     Problem,
     WORKLOADS,
     bf16_bits_from_f32,
+    make_activations,
     make_exact_problem,
     make_problem,
     seed_for,

@@ -193,3 +193,9 @@ def make_exact_problem(M: int, K: int, N: int, frac: float = 0.01, seed: int = 0
     return Problem(M, K, N, group, X, _pack_nibbles_along_axis0(codes), scales,
                    _pack_nibbles_along_axis1(z), kk.astype(np.int32),
                    nn.astype(np.int32), v, meta)
+
+
+def make_activations(M: int, K: int, seed: int) -> np.ndarray:
+    """bf16 bits of N(0,1) activations [M][K] (same recipe as make_problem's X)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return bf16_bits_from_f32(rng.standard_normal((M, K), dtype=np.float32))

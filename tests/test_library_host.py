@@ -1,0 +1,315 @@
+"""Host-side tests of libfq (no GPU): exports, Tile-COO packer against the
+oracle's independent packer, validation, and the C ABI's argument checks."""
+
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_15531_amd as fq
+from synth import make_problem
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fq.LIB_PATH):
+        from paper_2608_15531_amd.build import build
+        build()
+    return fq.load()
+
+
+def to_c_params(p: oracle.Params):
+    return {"k_tile": p.k_tile, "n_tile": p.n_tile, "buckets_per_tile": p.buckets,
+            "group_mode": p.group_mode, "reorder": p.reorder,
+            "elems_per_bank": p.elems_per_bank, "n_bank_groups": p.n_bank_groups}
+
+
+def test_exports_every_declared_symbol(lib):
+    with open(os.path.join(ROOT, "include", "fq.h")) as f:
+        header = f.read()
+    declared = set(re.findall(r"^\s*(?:fq_status|fq_tilecoo_params|const char\*)\s+(fq_\w+)\(",
+                              header, re.M))
+    assert declared, "no declarations parsed"
+    assert declared == set(fq.EXPORTS)
+    for name in declared:
+        assert getattr(lib, name) is not None
+
+
+def test_default_params(lib):
+    p = fq.fq_default_tilecoo_params().as_dict()
+    assert p == {"k_tile": 128, "n_tile": 64, "buckets_per_tile": 16, "group_mode": 0,
+                 "reorder": 3, "elems_per_bank": 2, "n_bank_groups": 4}
+
+
+def test_status_strings(lib):
+    for s in range(11):
+        assert fq.fq_status_string(s)
+    assert fq.fq_status_string(0) == "ok"
+
+
+PACK_CASES = [
+    (oracle.Params(), 1024, 512, 0.01, "uniform"),
+    (oracle.Params(), 512, 256, 0.05, "clustered"),
+    (oracle.Params(buckets=8), 512, 512, 0.02, "uniform"),
+    (oracle.Params(buckets=1), 256, 128, 0.03, "uniform"),
+    (oracle.Params(buckets=64, reorder=0), 512, 256, 0.02, "clustered"),
+    (oracle.Params(buckets=16, reorder=1), 512, 256, 0.02, "uniform"),
+    (oracle.Params(buckets=16, reorder=2), 512, 256, 0.02, "uniform"),
+    (oracle.Params(buckets=4, group_mode=1), 512, 256, 0.03, "clustered"),
+    (oracle.Params(buckets=5, group_mode=1, reorder=2), 512, 256, 0.03, "uniform"),
+    (oracle.Params(k_tile=64, n_tile=32, buckets=3, elems_per_bank=1, n_bank_groups=8),
+     512, 256, 0.02, "uniform"),
+    (oracle.Params(k_tile=256, n_tile=256, buckets=256), 512, 512, 0.01, "clustered"),
+    (oracle.Params(), 256, 128, 0.0, "uniform"),
+    (oracle.Params(), 128, 64, 1.0, "uniform"),
+]
+
+
+@pytest.mark.parametrize("case", PACK_CASES, ids=[f"case{i}" for i in range(len(PACK_CASES))])
+def test_pack_matches_oracle_bytes(lib, case):
+    p, K, N, frac, dist = case
+    prob = make_problem(1, K, N, frac=frac, seed=K + N + int(frac * 1000),
+                        dist=dist if frac < 0.5 else "uniform")
+    ref = oracle.pack_tile_coo(K, N, prob.k, prob.n, prob.v, p)
+    got = fq.fq_pack_tile_coo(K, N, prob.k, prob.n, prob.v, to_c_params(p))
+    assert np.array_equal(got.tile_indptr, ref.tile_indptr)
+    assert np.array_equal(got.bucket_info, ref.bucket_info)
+    assert np.array_equal(got.packed, ref.packed)
+    s = got.sizes
+    assert s.n_tiles == ref.n_tiles and s.n_buckets == ref.n_buckets
+    assert s.n_groups == ref.n_groups and s.nnz == prob.nnz
+    assert s.n_pad == 4 * s.n_groups - s.nnz and s.bytes == ref.bytes
+    per_tile = np.diff(ref.tile_indptr.astype(np.int64))
+    assert s.max_tile_groups == (per_tile.max() if per_tile.size else 0)
+    # host decode round trip, and the oracle's decode of the library's bytes
+    k, n, v = fq.fq_unpack_tile_coo(K, N, to_c_params(p), got.tile_indptr, got.bucket_info,
+                                    got.packed)
+    ek, en, ev = oracle.coo_sorted(prob.k, prob.n, prob.v)
+    assert np.array_equal(k, ek) and np.array_equal(n, en) and np.array_equal(v, ev)
+    fq.fq_validate_tile_coo(K, N, to_c_params(p), got.tile_indptr, got.bucket_info, got.packed)
+
+
+def test_pack_order_independent(lib):
+    prob = make_problem(1, 512, 256, frac=0.02, seed=3)
+    a = fq.fq_pack_tile_coo(512, 256, prob.k, prob.n, prob.v)
+    perm = np.random.default_rng(0).permutation(prob.nnz)
+    b = fq.fq_pack_tile_coo(512, 256, prob.k[perm], prob.n[perm], prob.v[perm])
+    assert np.array_equal(a.packed, b.packed) and np.array_equal(a.bucket_info, b.bucket_info)
+
+
+def test_pack_hand_fixture(lib):
+    import json
+    with open(os.path.join(ROOT, "tests", "golden", "tilecoo_hand.json")) as f:
+        g = json.load(f)
+    k = np.array([e[0] for e in g["coo"]])
+    n = np.array([e[1] for e in g["coo"]])
+    v = np.array([int(e[2], 16) for e in g["coo"]], dtype=np.uint16)
+    for case in g["cases"]:
+        pr = dict(case["params"])
+        pr["buckets_per_tile"] = pr.pop("buckets")
+        got = fq.fq_pack_tile_coo(g["K"], g["N"], k, n, v, pr)
+        assert got.tile_indptr.tolist() == case["tile_indptr"]
+        assert got.bucket_info.tolist() == case["bucket_info"]
+        words = []
+        for ks, ns, vs in case["groups"]:
+            vb = [int(x, 16) for x in vs]
+            words += [ks[0] | ks[1] << 8 | ks[2] << 16 | ks[3] << 24,
+                      ns[0] | ns[1] << 8 | ns[2] << 16 | ns[3] << 24,
+                      vb[0] | vb[1] << 16, vb[2] | vb[3] << 16]
+        assert got.packed.tolist() == words
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(k=[0, 0], n=[1, 1], v=[1, 2]), "FQ_ERR_DUPLICATE"),
+    (dict(k=[256], n=[1], v=[1]), "FQ_ERR_RANGE"),
+    (dict(k=[-1], n=[1], v=[1]), "FQ_ERR_RANGE"),
+    (dict(k=[1], n=[128], v=[1]), "FQ_ERR_RANGE"),
+    (dict(k=[1], n=[1], v=[0x8000]), "FQ_ERR_ZERO_VALUE"),
+    (dict(k=[1], n=[1], v=[0]), "FQ_ERR_ZERO_VALUE"),
+])
+def test_pack_rejects_bad_coo(lib, bad, status):
+    with pytest.raises(fq.FqError) as e:
+        fq.fq_pack_tile_coo(256, 128, np.array(bad["k"]), np.array(bad["n"]),
+                            np.array(bad["v"], dtype=np.uint16))
+    assert e.value.name == status
+
+
+@pytest.mark.parametrize("params,K,N,status", [
+    ({"k_tile": 300}, 600, 128, "FQ_ERR_FORMAT"),
+    ({"n_tile": 0}, 256, 128, "FQ_ERR_FORMAT"),
+    ({}, 250, 128, "FQ_ERR_SHAPE"),
+    ({}, 256, 100, "FQ_ERR_SHAPE"),
+    ({"buckets_per_tile": 0}, 256, 128, "FQ_ERR_FORMAT"),
+    ({"group_mode": 2}, 256, 128, "FQ_ERR_FORMAT"),
+    ({"reorder": 4}, 256, 128, "FQ_ERR_FORMAT"),
+    ({"elems_per_bank": 64, "n_bank_groups": 4}, 256, 128, "FQ_ERR_FORMAT"),
+])
+def test_pack_rejects_bad_params(lib, params, K, N, status):
+    with pytest.raises(fq.FqError) as e:
+        fq.fq_pack_tile_coo(K, N, np.array([1]), np.array([1]), np.array([1], np.uint16), params)
+    assert e.value.name == status
+
+
+def test_pack_null_arguments(lib):
+    sizes = fq.fq_tilecoo_sizes()
+    p = fq.fq_default_tilecoo_params()
+    k = np.array([1], np.int32)
+    v = np.array([1], np.uint16)
+    assert lib.fq_pack_tile_coo(256, 128, 1, None, k.ctypes.data, v.ctypes.data, C.byref(p),
+                                C.byref(sizes), None, None, None) == 1
+    assert lib.fq_pack_tile_coo(256, 128, 1, k.ctypes.data, k.ctypes.data, v.ctypes.data,
+                                C.byref(p), None, None, None, None) == 1
+    ti = np.zeros(16, np.uint32)
+    assert lib.fq_pack_tile_coo(256, 128, 1, k.ctypes.data, k.ctypes.data, v.ctypes.data,
+                                C.byref(p), C.byref(sizes), ti.ctypes.data, None, None) == 1
+    # NULL params -> defaults
+    assert lib.fq_pack_tile_coo(256, 128, 1, k.ctypes.data, k.ctypes.data, v.ctypes.data,
+                                None, C.byref(sizes), None, None, None) == 0
+    assert sizes.n_tiles == 4 and sizes.n_groups == 1 and sizes.n_pad == 3
+
+
+def _corrupt_cases(tc):
+    ti, bi, pk = tc.tile_indptr.copy(), tc.bucket_info.copy(), tc.packed.copy()
+    yield "indptr_start", (ti + np.uint32(1)), bi, pk
+    t2 = ti.copy(); t2[1], t2[2] = t2[2], t2[1]
+    if t2[1] != ti[1]:
+        yield "indptr_order", t2, bi, pk
+    b2 = bi.copy(); b2[1] += 1
+    yield "bucket_count", ti, b2, pk
+    b3 = bi.copy(); b3[2] += 1
+    yield "bucket_offset", ti, b3, pk
+    p2 = pk.copy(); p2[0] |= 0x80   # row 128+ in a 128-row tile
+    yield "row_range", ti, bi, p2
+    p3 = pk.copy(); p3[1] = (p3[1] & 0xFFFFFF00) | 0x40   # column 64 in a 64-column tile
+    yield "col_range", ti, bi, p3
+    p4 = pk.copy(); p4[1] = (p4[1] & 0xFFFFFF00) | ((p4[1] + 1) & 0x3F)   # split one group
+    yield "group_column", ti, bi, p4
+    # duplicate position: copy slot 0 of group 0 onto slot 0 of group 1 (same tile)
+    p5 = pk.copy().reshape(-1, 4)
+    p5[1] = p5[0]
+    yield "duplicate", ti, bi, p5.ravel()
+
+
+def test_validate_rejects_corruption(lib):
+    prob = make_problem(1, 512, 256, frac=0.03, seed=17)
+    tc = fq.fq_pack_tile_coo(512, 256, prob.k, prob.n, prob.v)
+    fq.fq_validate_tile_coo(512, 256, None, tc.tile_indptr, tc.bucket_info, tc.packed)
+    names = []
+    for name, ti, bi, pk in _corrupt_cases(tc):
+        with pytest.raises(fq.FqError) as e:
+            fq.fq_validate_tile_coo(512, 256, None, ti, bi, pk)
+        assert e.value.name == "FQ_ERR_FORMAT", name
+        names.append(name)
+    assert len(names) >= 7
+
+
+def test_validate_rejects_shared_column(lib):
+    # two buckets of one tile claiming the same column
+    p = {"k_tile": 8, "n_tile": 4, "buckets_per_tile": 2, "elems_per_bank": 2,
+         "n_bank_groups": 4}
+    tc = fq.fq_pack_tile_coo(8, 4, np.array([0, 1]), np.array([0, 1]),
+                             np.array([0x3F80, 0x4000], np.uint16), p)
+    pk = tc.packed.copy().reshape(-1, 4)
+    assert pk.shape[0] == 2
+    pk[1, 1] = pk[0, 1]    # second bucket's group now names the first bucket's column
+    pk[1, 0] = 0x07070707 & pk[1, 0] | 0x05050505   # keep rows distinct from group 0
+    with pytest.raises(fq.FqError):
+        fq.fq_validate_tile_coo(8, 4, p, tc.tile_indptr, tc.bucket_info, pk.ravel())
+
+
+def test_storage_formula_on_library_output(lib):
+    prob = make_problem(1, 4096, 4096, frac=0.01, seed=0)
+    tc = fq.fq_pack_tile_coo(4096, 4096, prob.k, prob.n, prob.v)
+    s = tc.sizes
+    assert s.n_tiles == 2048 and s.n_buckets == 2048 * 16 and s.nnz == 167772
+    assert s.bytes == oracle.storage_bytes(s.n_tiles, s.n_buckets, 4 * s.n_groups)
+    # padded Tile-COO still beats the paper's CSR count at 1 %
+    assert s.bytes < oracle.csr_bytes(4096, s.nnz)
+
+
+# ---------------------------------------------------- device entry points --
+# Only argument checks that fail before any launch are exercised here.
+
+def _problem(**kw):
+    d = dict(M=4, K=1024, N=512, group_size=128, y_dtype=0, split_k=0)
+    d.update(kw)
+    return fq.fq_problem(**d)
+
+
+FAKE = 1 << 20   # 16-byte aligned, never dereferenced: validation fails first
+
+
+def _tc(**kw):
+    p = fq.fq_default_tilecoo_params()
+    for k, v in kw.pop("params", {}).items():
+        setattr(p, k, v)
+    d = dict(tile_indptr=FAKE, bucket_info=FAKE, packed=FAKE, params=p, n_groups=10,
+             max_tile_groups=2)
+    d.update(kw)
+    return fq.fq_tilecoo_dev(**d)
+
+
+def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, wsb=1 << 30):
+    tc = tc if tc is not None else _tc()
+    return fq.STATUS_NAMES[lib.fq_w4a16_outlier_matmul(C.byref(pr), X, Wq, s, z, C.byref(tc),
+                                                       Y, ws, wsb, None)]
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(M=0), "FQ_ERR_SHAPE"),
+    (dict(M=33), "FQ_ERR_UNSUPPORTED"),
+    (dict(K=1000), "FQ_ERR_SHAPE"),
+    (dict(N=96), "FQ_ERR_SHAPE"),
+    (dict(group_size=64), "FQ_ERR_UNSUPPORTED"),
+    (dict(y_dtype=5), "FQ_ERR_UNSUPPORTED"),
+    (dict(split_k=-1), "FQ_ERR_SHAPE"),
+])
+def test_matmul_rejects_bad_problem(lib, kw, status):
+    assert _call(lib, _problem(**kw)) == status
+
+
+def test_matmul_rejects_bad_pointers(lib):
+    pr = _problem()
+    assert _call(lib, pr, X=None) == "FQ_ERR_NULL"
+    assert _call(lib, pr, Y=None) == "FQ_ERR_NULL"
+    assert _call(lib, pr, X=FAKE + 2) == "FQ_ERR_ALIGN"
+    assert _call(lib, pr, Wq=FAKE + 4) == "FQ_ERR_ALIGN"
+    assert _call(lib, pr, s=FAKE + 2) == "FQ_ERR_ALIGN"
+    assert _call(lib, pr, Y=FAKE + 8) == "FQ_ERR_ALIGN"
+    assert lib.fq_w4a16_outlier_matmul(C.byref(pr), FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                                       1 << 30, None) == 1
+
+
+def test_matmul_rejects_bad_tilecoo(lib):
+    pr = _problem()
+    assert _call(lib, pr, tc=_tc(params={"k_tile": 64})) == "FQ_ERR_UNSUPPORTED"
+    assert _call(lib, pr, tc=_tc(params={"n_tile": 128})) == "FQ_ERR_UNSUPPORTED"
+    assert _call(lib, pr, tc=_tc(params={"buckets_per_tile": 512})) == "FQ_ERR_UNSUPPORTED"
+    assert _call(lib, pr, tc=_tc(packed=None)) == "FQ_ERR_NULL"
+    assert _call(lib, pr, tc=_tc(packed=FAKE + 8)) == "FQ_ERR_ALIGN"
+    assert _call(lib, pr, tc=_tc(n_groups=-1)) == "FQ_ERR_FORMAT"
+
+
+def test_matmul_rejects_small_workspace(lib):
+    pr = _problem(N=4096, K=4096)
+    need = C.c_size_t(0)
+    assert lib.fq_workspace_bytes(C.byref(pr), C.byref(need)) == 0
+    assert need.value > 0
+    assert _call(lib, pr, wsb=need.value - 1) == "FQ_ERR_WORKSPACE"
+    assert _call(lib, pr, ws=None) == "FQ_ERR_WORKSPACE"
+    assert _call(lib, pr, ws=FAKE + 16) == "FQ_ERR_WORKSPACE"
+    un = C.c_size_t(0)
+    assert lib.fq_workspace_bytes_unfused(C.byref(pr), C.byref(un)) == 0
+    assert un.value >= need.value + 4 * 4 * 4096
+
+
+def test_debug_decode_rejects(lib):
+    tc = _tc()
+    assert lib.fq_debug_decode_tile_coo(None, 256, 128, FAKE, FAKE, FAKE, None) == 1
+    assert lib.fq_debug_decode_tile_coo(C.byref(tc), 250, 128, FAKE, FAKE, FAKE, None) == 2
+    assert lib.fq_debug_decode_tile_coo(C.byref(tc), 256, 128, None, FAKE, FAKE, None) == 1
