@@ -179,6 +179,8 @@ typedef struct {
  *   group_size  G, must be 128 (one group per 128 x 64 tile).
  *   y_dtype     FQ_Y_BF16 (round to nearest even once, after the full sum) or FQ_Y_F32.
  *   split_k     number of K ranges per 64-column strip; 0 lets the library choose.
+ *   flags       0, or one FQ_SPARSE_* value to force the sparse-path mapping
+ *               (the library otherwise picks by M).
  */
 typedef struct {
   int32_t M;
@@ -187,14 +189,23 @@ typedef struct {
   int32_t group_size;
   int32_t y_dtype;
   int32_t split_k;
+  int32_t flags;
 } fq_problem;
+
+/* Sparse-path mappings (fq_problem.flags).  GATHER: each lane decodes one
+ * 16-byte group and gathers X[m][k] from LDS for every row (VALU dot2).
+ * MFMA: the tile's outliers are scattered into an LDS image of the MFMA B
+ * operand and multiplied on the matrix cores.  Both are exact in fp32. */
+enum { FQ_SPARSE_AUTO = 0, FQ_SPARSE_GATHER = 1, FQ_SPARSE_MFMA = 2 };
 
 /*
  * fq_workspace_bytes -- device workspace the matmul entry points need for
- * problem pr.  The workspace holds split-K partial sums (scratch, rewritten by
- * every call) and per-strip arrival counters.  Zero-fill it once before its
- * first use; every call returns the counters to zero, so no per-call clearing
- * is needed.  Calls that may overlap in time need separate workspaces.
+ * problem pr.  Its first 256 KiB hold one arrival counter per 64-column strip
+ * (so N <= 4194304); the rest holds split-K partial sums and is scratch,
+ * rewritten by every call.  Zero-fill the workspace once before its first use;
+ * every call returns the counters to zero, so no per-call clearing is needed
+ * and one workspace may serve problems of any shape in turn.  Calls that may
+ * overlap in time need separate workspaces.
  */
 fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes);
 

@@ -30,6 +30,10 @@ FQ_REORDER_COLUMNS = 1
 FQ_REORDER_ELEMENTS = 2
 FQ_Y_BF16 = 0
 FQ_Y_F32 = 1
+FQ_SPARSE_AUTO = 0
+FQ_SPARSE_GATHER = 1
+FQ_SPARSE_MFMA = 2
+_SPARSE_MODES = {"auto": FQ_SPARSE_AUTO, "gather": FQ_SPARSE_GATHER, "mfma": FQ_SPARSE_MFMA}
 
 
 class FqError(RuntimeError):
@@ -65,7 +69,8 @@ class fq_tilecoo_dev(C.Structure):
 
 class fq_problem(C.Structure):
     _fields_ = [("M", C.c_int32), ("K", C.c_int32), ("N", C.c_int32),
-                ("group_size", C.c_int32), ("y_dtype", C.c_int32), ("split_k", C.c_int32)]
+                ("group_size", C.c_int32), ("y_dtype", C.c_int32), ("split_k", C.c_int32),
+                ("flags", C.c_int32)]
 
 
 _lib = None
@@ -254,8 +259,8 @@ def workspace(nbytes: int, device, stream_handle: int):
     return buf
 
 
-def _problem(M, K, N, y_dtype, split_k, group=128) -> fq_problem:
-    return fq_problem(M, K, N, group, y_dtype, split_k)
+def _problem(M, K, N, y_dtype, split_k, group=128, sparse="auto") -> fq_problem:
+    return fq_problem(M, K, N, group, y_dtype, split_k, _SPARSE_MODES[sparse])
 
 
 def _check_tensor(t, dtype, shape, name):
@@ -285,11 +290,12 @@ def _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group):
 
 
 def fq_w4a16_outlier_matmul(X, Wq, scales, zeros, tc: TileCOODevice, Y=None, y_dtype="bf16",
-                            split_k: int = 0, stream=None, ws=None, group: int = 128):
+                            split_k: int = 0, stream=None, ws=None, group: int = 128,
+                            sparse: str = "auto"):
     """Fused Y = X dequant(W_Q) + X W_O on the GPU; returns Y."""
     lib = load()
     M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
-    pr = _problem(M, K, N, ydt, split_k, group)
+    pr = _problem(M, K, N, ydt, split_k, group, sparse)
     need = C.c_size_t(0)
     _check(lib.fq_workspace_bytes(C.byref(pr), C.byref(need)), "fq_workspace_bytes")
     sh = _stream_handle(stream, X.device)
@@ -305,11 +311,11 @@ def fq_w4a16_outlier_matmul(X, Wq, scales, zeros, tc: TileCOODevice, Y=None, y_d
 
 def fq_w4a16_outlier_matmul_unfused(X, Wq, scales, zeros, tc: TileCOODevice, Y=None,
                                     y_dtype="bf16", split_k: int = 0, stream=None, ws=None,
-                                    group: int = 128):
+                                    group: int = 128, sparse: str = "auto"):
     """Two-kernel baseline (dense W4A16 then Tile-COO SpMM); returns Y."""
     lib = load()
     M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
-    pr = _problem(M, K, N, ydt, split_k, group)
+    pr = _problem(M, K, N, ydt, split_k, group, sparse)
     need = C.c_size_t(0)
     _check(lib.fq_workspace_bytes_unfused(C.byref(pr), C.byref(need)),
            "fq_workspace_bytes_unfused")

@@ -16,6 +16,8 @@ fq_status check_problem(const fq_problem* pr) {
   if (pr->group_size != fqi::kTileK) return FQ_ERR_UNSUPPORTED;
   if (pr->M > fqi::kMaxM) return FQ_ERR_UNSUPPORTED;
   if (pr->y_dtype != FQ_Y_BF16 && pr->y_dtype != FQ_Y_F32) return FQ_ERR_UNSUPPORTED;
+  if (pr->flags < FQ_SPARSE_AUTO || pr->flags > FQ_SPARSE_MFMA) return FQ_ERR_UNSUPPORTED;
+  if (pr->flags == FQ_SPARSE_GATHER && pr->M > 16) return FQ_ERR_UNSUPPORTED;
   return FQ_OK;
 }
 
@@ -48,9 +50,10 @@ fq_status run(const fq_problem* pr, const uint16_t* X, const uint32_t* Wq,
               void* workspace, size_t workspace_bytes, void* stream, bool dense, bool sparse,
               const float* y_addend) {
   fqi::Plan plan;
+  const int mode = pr->flags == FQ_SPARSE_GATHER ? 0 : pr->flags == FQ_SPARSE_MFMA ? 1 : -1;
   if (!fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, dense, sparse,
                       sparse ? tc->params.buckets_per_tile : 0,
-                      sparse ? tc->max_tile_groups : 0, &plan))
+                      sparse ? tc->max_tile_groups : 0, &plan, mode))
     return FQ_ERR_UNSUPPORTED;
   if (!workspace) return FQ_ERR_WORKSPACE;
   if (workspace_bytes < plan.ws_bytes || !aligned(workspace, 256)) return FQ_ERR_WORKSPACE;

@@ -12,29 +12,36 @@ constexpr int kTileN = 64;      // N side of a tile = one output strip
 constexpr int kThreads = 256;   // four wave64 per workgroup
 constexpr int kMaxM = 32;       // rows the fused GEMV-regime kernel supports
 constexpr int kMaxBuckets = 256;
+constexpr int kXStride = 136;   // LDS row stride (elements) of a staged 128-wide X slice
+constexpr int kGatherMaxM = 4;  // up to this M the sparse path gathers X in LDS; above, MFMA
+// The workspace starts with a fixed counter region (one uint32 per 64-column
+// strip, zero between calls) so that a workspace shared by problems of
+// different shapes never finds partial sums where a counter is expected.
+constexpr size_t kCounterRegion = 256 * 1024;
+constexpr int kMaxStrips = int(kCounterRegion / 4);
 
 // Launch plan of one matmul kernel.  Everything that sizes the workspace
 // depends only on (M, K, N, split_k) so the workspace can be sized before the
 // Tile-COO exists.
 struct Plan {
   int M, K, N;
-  int MB;            // 16-row blocks: 1 (M <= 16) or 2 (M <= 32)
+  int MB;            // 16-row MFMA blocks: 1 (M <= 16) or 2 (M <= 32)
+  int MODE;          // sparse mapping: 0 LDS gathers (M <= kGatherMaxM), 1 MFMA
   int n_strips;      // N / 64
   int T;             // tiles per strip, K / 128
   int S;             // K ranges per strip (split-K)
-  int nt_max;        // most tiles one workgroup covers
-  int xstride;       // LDS row stride of the staged activations, elements
   int B;             // buckets per tile
-  int stage_cap;     // Tile-COO groups the LDS stage holds
-  // dynamic LDS layout, bytes
-  size_t off_xsum, off_shc, off_stage, off_binfo, off_tptr, off_flag, lds_bytes;
-  // workspace layout, bytes
-  size_t partial_bytes, counter_offset, ws_bytes;
+  // dynamic LDS layout, bytes: four wave slots (X slice or B-operand image),
+  // then the gather-mode sparse output buffers
+  size_t slot_bytes, off_shc, off_flag, lds_bytes;
+  // workspace layout, bytes: counters at 0, partial sums at kCounterRegion
+  size_t partial_bytes, ws_bytes;
 };
 
 // Returns false when (M, K, N) is outside what the kernels implement.
+// mode: -1 picks the sparse mapping by M, 0 forces gathers, 1 forces MFMA.
 bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
-               int64_t max_tile_groups, Plan* plan);
+               int64_t max_tile_groups, Plan* plan, int mode = -1);
 
 struct MatmulPtrs {
   const uint16_t* X;

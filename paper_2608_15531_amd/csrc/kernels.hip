@@ -2,35 +2,44 @@
 // halves, and the Tile-COO group decoder.
 //
 // One workgroup = four wave64 = one 64-column output strip x one contiguous K
-// range of 128-row tiles (FlashQuant Sec. 3.1, CTA level: the dense and sparse
-// work of the same output tile share a workgroup and its on-chip X tile).
+// range of 128-row tiles (FlashQuant Sec. 3.1, CTA level: the dense and the
+// sparse work of the same output tile run in the same workgroup and
+// accumulate into the same register output tile).  Each wave streams its own
+// contiguous run of tiles with no workgroup barrier in the loop.
 //
-//   phase A  the K range of X is copied once into LDS (row-major, each
-//            8-element chunk permuted to the MFMA operand order), together
-//            with the per-(tile, row) sums of X, the workgroup's slice of
-//            tile_indptr and bucket_info, and its contiguous Tile-COO segment
-//            (Sec. 3.2.1: tiles of one strip are contiguous).  The first
-//            weight tile of every wave is already in flight.
-//   dense    waves split the K range tile by tile (Sec. 3.1, warp level:
-//            sliced K).  Per tile a lane holds 16 bytes of packed INT4 per
-//            32-row step (one 128-bit load), converts them in registers to
-//            bf16 operands and issues v_mfma_f32_16x16x32_bf16 against the
-//            LDS-resident X; scales and zero-points are applied in fp32 once
-//            per 128-row group.  The next tile's weights, scales and zeros are
-//            loaded while the current one is computed (Sec. 4.1 pipeline).
-//   sparse   every lane of the workgroup owns one (tile slot, bucket) pair,
-//            walks its bucket's 16-byte groups from the LDS stage, gathers
-//            X[m][k] from the same LDS tile and accumulates v * x with
-//            v_dot2_f32_bf16 into an LDS output buffer (Sec. 3.1 thread level,
-//            Sec. 4.2 decoding).  Within a tile every bucket owns whole
-//            columns; lanes working on different tiles of the strip may touch
-//            the same column, so the buffer update is the LDS unit's
-//            single-instruction float add.
-//   reduce   wave partials and the sparse buffer are summed in LDS in a fixed
-//            order; with split-K each workgroup stores its fp32 partial and the
-//            last one to arrive at the strip's counter adds all partials in
-//            split order and writes Y (Sec. 3.1 Stream-K reduction), then
-//            rearms the counter for the next call.
+//   prefetch  two register buffers alternate, each holding one tile: 16 bytes
+//             of packed INT4 per lane and 32-row step (one 128-bit load each),
+//             the fp16 scales and INT4 zero-points of the lane's four columns,
+//             the tile's slice of X (from L2), and the tile's Tile-COO groups,
+//             one 16-byte group per lane (the tiles of a strip are stored
+//             contiguously, so one load of tile_indptr gives every range).
+//             While tile t is computed, tile t+1 is in flight (Sec. 4.1).
+//   dense     per 32-row step a lane turns 8 codes of each of its 4 columns
+//             into bf16 (16 + q) operands in registers and issues
+//             v_mfma_f32_16x16x32_bf16 against X; one more MFMA against an
+//             all-ones operand yields the per-row sums of X.  After the group:
+//             acc += s * (sum x (16+q) - (16+z) sum x), i.e. eq. (3) applied
+//             exactly once per (group, column) in fp32.
+//   sparse    (Sec. 3.1 thread level, Sec. 4.2 decoding) two mappings of the
+//             same Tile-COO groups, chosen by the number of rows M:
+//     M <= 4  the tile's X slice sits in the wave's LDS slot; each lane decodes
+//             one group, gathers X[m][k] for every row and accumulates v * x
+//             with v_dot2_f32_bf16 into the wave's LDS output buffer.
+//     M >= 5  each lane scatters its group's values into an LDS buffer laid out
+//             as the MFMA B operand of the tile (zero elsewhere); the wave reads
+//             it back with conflict-free 128-bit reads and issues 16 MFMAs
+//             against the same X fragments straight into the register output
+//             tile, then restores the zeros.  bf16 x bf16 products are exact in
+//             the fp32 accumulator, so this is the SpMM of eq. (1) on the
+//             matrix cores, with its cost independent of M.
+//   reduce    after the loop the four waves' register tiles (and sparse
+//             buffers) are summed in LDS in a fixed order.  With split-K each
+//             workgroup stores its fp32 partial with device-coherent stores
+//             and the last to arrive at the strip's counter adds all partials
+//             in split order and writes Y (Sec. 3.1 Stream-K reduction), then
+//             rearms the counter.  Only the partials and the counter cross
+//             workgroups, through agent-scope atomic accesses, so no
+//             cache-wide fence is issued.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -40,13 +49,14 @@
 
 namespace fqk {
 
+constexpr int XS = fqi::kXStride;   // LDS row stride of a staged X slice, elements
+
 struct MatmulArgs {
   const uint16_t* X;
   const uint32_t* Wq;
   const uint16_t* scales;
   const uint32_t* zeros;
   const uint32_t* tile_indptr;
-  const uint32_t* bucket_info32;  // one (offset | count << 16) word per bucket
   const uint4* packed;
   const float* y_addend;
   void* Y;
@@ -56,26 +66,77 @@ struct MatmulArgs {
   int M, K, N;
   int y_f32;
   int T, S;
-  int xstride;
-  int B;
-  int stage_cap;
-  int off_xsum, off_shc, off_stage, off_binfo, off_tptr, off_flag;
+  int slot_bytes;      // one wave's LDS slot
+  int off_shc;         // per-wave sparse output buffers (gather mode)
+  int off_flag;
 };
 
+// Global loads one tile costs in each mode (each counts once in vmcnt).
+template <int MB, int MODE, bool DENSE, bool SPARSE>
+constexpr int loads_per_tile() {
+  return (DENSE ? 6 : 0) + (MODE == 0 ? 1 : 4 * MB) + (SPARSE ? 2 : 0);
+}
+
+// Everything one wave needs for one tile, held in registers until used.
+template <int MB, int MODE>
 struct TileRegs {
-  uint4 w[4];      // packed codes: rows t*16 + 4*step + h, columns n0 + 4*c4 .. +3
+  static constexpr int NX = MODE == 0 ? 1 : 4 * MB;
+  uint4 w[4];      // codes: rows 16t + 4*step + h, columns n0 + 4*c4 .. +3
   uint2 s;         // fp16 scales of those four columns
   uint32_t z;      // zero-point word holding those four columns
+  uint4 x[NX];     // MODE 0: X chunk lane (row lane/16, elements 8*(lane%16)..+7)
+                   // MODE 1: A fragment [mb][step]: row 16mb + c4, elements 32step + 8h..+7
+  uint4 g[2];      // Tile-COO groups lane and lane + 64 of the tile
+  uint32_t g0, g1; // the tile's group range
 };
 
-__device__ __forceinline__ void load_tile(const MatmulArgs& a, int t, int n0, int h, int c4,
-                                          TileRegs& r) {
-  const uint32_t* base = a.Wq + size_t(t * 16 + h) * a.N + n0 + 4 * c4;
+template <int MB, int MODE, bool DENSE, bool SPARSE>
+__device__ __forceinline__ void load_tile(const MatmulArgs& a, int t, int n0, int lane,
+                                          uint32_t g0, uint32_t g1, TileRegs<MB, MODE>& r) {
+  // Every load is unconditional (addresses clamped into range) so the
+  // compiler counts outstanding loads exactly across the prefetch.
+  const int h = lane >> 4;
+  const int c4 = lane & 15;
+  if (DENSE) {
+    const uint32_t* base = a.Wq + size_t(t * 16 + h) * a.N + n0 + 4 * c4;
 #pragma unroll
-  for (int step = 0; step < 4; ++step)
-    r.w[step] = *reinterpret_cast<const uint4*>(base + size_t(4 * step) * a.N);
-  r.s = *reinterpret_cast<const uint2*>(a.scales + size_t(t) * a.N + n0 + 4 * c4);
-  r.z = a.zeros[size_t(t) * (a.N >> 3) + ((n0 + 4 * c4) >> 3)];
+    for (int step = 0; step < 4; ++step)
+      r.w[step] = *reinterpret_cast<const uint4*>(base + size_t(4 * step) * a.N);
+    r.s = *reinterpret_cast<const uint2*>(a.scales + size_t(t) * a.N + n0 + 4 * c4);
+    r.z = a.zeros[size_t(t) * (a.N >> 3) + ((n0 + 4 * c4) >> 3)];
+  }
+  if (MODE == 0) {
+    const int m = min(lane >> 4, a.M - 1);
+    r.x[0] = *reinterpret_cast<const uint4*>(a.X + size_t(m) * a.K + t * 128 + 8 * (lane & 15));
+  } else {
+    // Rows past M load row M-1; their output rows are never stored.
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int m = min(mb * 16 + c4, a.M - 1);
+      const uint16_t* row = a.X + size_t(m) * a.K + t * 128 + 8 * h;
+#pragma unroll
+      for (int step = 0; step < 4; ++step)
+        r.x[mb * 4 + step] = *reinterpret_cast<const uint4*>(row + 32 * step);
+    }
+  }
+  if (SPARSE) {
+    r.g0 = g0;
+    r.g1 = g1;
+    // Lanes past the tile's last group reload that group (same cache line),
+    // never another tile's.  An empty tile reads group g0, which is in range:
+    // with no outliers at all `packed` points at valid scratch.
+    const uint32_t last = g1 > g0 ? g1 - 1 : g0;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) r.g[j] = a.packed[min(g0 + uint32_t(lane + 64 * j), last)];
+  }
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt low bits [3:0], high bits [15:14]; expcnt and lgkmcnt left at max).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
 __device__ __forceinline__ void store_out(const MatmulArgs& a, int m, int n, f32x4_t v) {
@@ -94,20 +155,77 @@ __device__ __forceinline__ void store_out(const MatmulArgs& a, int m, int n, f32
   }
 }
 
-template <int MB, bool DENSE, bool SPARSE>
+// Gather mode: one group held by this lane, all rows, into the wave's buffer.
+__device__ __forceinline__ void sparse_gather(const MatmulArgs& a, const uint16_t* xs, uint4 raw,
+                                              float* shc) {
+  const Group d = decode_group(raw);
+  const uint32_t p4 = chunk_pos4(d.rows & 0x7F7F7F7Fu);
+  const uint32_t p0 = p4 & 0xFFu, p1 = (p4 >> 8) & 0xFFu;
+  const uint32_t p2 = (p4 >> 16) & 0xFFu, p3 = p4 >> 24;
+  if (single_column(d)) {
+    float* out = shc + (d.cols & 63u);
+    for (int m0 = 0; m0 < a.M; m0 += 4) {
+      // four rows at a time: all sixteen gathers issued before any use
+      uint32_t x01[4], x23[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint16_t* xr = xs + min(m0 + j, a.M - 1) * XS;
+        x01[j] = uint32_t(xr[p0]) | (uint32_t(xr[p1]) << 16);
+        x23[j] = uint32_t(xr[p2]) | (uint32_t(xr[p3]) << 16);
+      }
+      float part[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) part[j] = dot2_bf16(x23[j], d.v23, dot2_bf16(x01[j], d.v01, 0.f));
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (m0 + j < a.M) atomicAdd(out + (m0 + j) * 64, part[j]);
+    }
+  } else {
+    const uint32_t pj[4] = {p0, p1, p2, p3};
+    for (int m = 0; m < a.M; ++m) {
+      const uint16_t* xr = xs + m * XS;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t v = slot_val(d, j);
+        if (v != 0u)
+          atomicAdd(shc + m * 64 + (slot_col(d, j) & 63u),
+                    bf16_bits_to_f32(xr[pj[j]]) * bf16_bits_to_f32(v));
+      }
+    }
+  }
+}
+
+// MFMA mode: write (or clear) a group's real values into the wave's B-operand
+// image of the tile.  Element (k, n) of the tile lives where lane
+// (n/4 + 16 * ((k%32)/8)) reads B of MFMA (step k/32, column block n%4), at
+// the element the X fragment holds k at (chunk order x0,x4,x1,x5,...).
+__device__ __forceinline__ void scatter_group(uint16_t* bo, uint4 raw, bool clear) {
+  const Group d = decode_group(raw);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t v = slot_val(d, j);
+    if (v == 0u) continue;   // padding slots may share a real slot's position
+    const uint32_t k = slot_row(d, j) & 127u;
+    const uint32_t n = slot_col(d, j) & 63u;
+    const uint32_t lane = (n >> 2) + 16u * ((k >> 3) & 3u);
+    const uint32_t blk = (k >> 5) * 4u + (n & 3u);
+    bo[(blk * 64u + lane) * 8u + chunk_pos(k & 7u)] = clear ? uint16_t(0) : uint16_t(v);
+  }
+}
+
+template <int MB, int MODE, bool DENSE, bool SPARSE>
 __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int MR = MB * 16;                 // rows of the register output tile
-  constexpr int RED_SLOTS = (MB <= 2) ? 4 : 1;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  // wave-uniform: keeps the tile loop in scalar control flow
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int h = lane >> 4;                     // k-chunk of the MFMA operands
   const int c4 = lane & 15;                    // MFMA column / A row
 
   // Workgroups are dealt round-robin to the eight XCDs; give each XCD a
-  // contiguous run of (strip, split) pairs so the splits of one strip share
-  // an L2.
+  // contiguous run of (strip, split) pairs so the splits of one strip and
+  // neighbouring strips share an L2.
   const int G = gridDim.x;
   const int bid = blockIdx.x;
   const int logical = (G & 7) == 0 ? (bid & 7) * (G >> 3) + (bid >> 3) : bid;
@@ -116,203 +234,193 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
   const int t_lo = int(int64_t(split) * a.T / a.S);
   const int t_hi = int(int64_t(split + 1) * a.T / a.S);
   const int nt = t_hi - t_lo;
+  const int w_lo = t_lo + (nt * wave) / 4;     // this wave's tiles [w_lo, w_hi)
+  const int w_hi = t_lo + (nt * (wave + 1)) / 4;
   const int n0 = strip * 64;
-  const int k0 = t_lo * 128;
-  const int64_t tile0 = int64_t(strip) * a.T + t_lo;
+  const int64_t tile_base = int64_t(strip) * a.T;
 
-  uint16_t* Xs = reinterpret_cast<uint16_t*>(smem);
-  float* red = reinterpret_cast<float*>(smem);   // reuses the X region after both paths
-  float* Xsum = reinterpret_cast<float*>(smem + a.off_xsum);
-  float* shc = reinterpret_cast<float*>(smem + a.off_shc);
-  uint4* stage = reinterpret_cast<uint4*>(smem + a.off_stage);
-  uint32_t* binfo = reinterpret_cast<uint32_t*>(smem + a.off_binfo);
-  uint32_t* tptr = reinterpret_cast<uint32_t*>(smem + a.off_tptr);
+  unsigned char* slot = smem + size_t(wave) * a.slot_bytes;
+  uint16_t* xs = reinterpret_cast<uint16_t*>(slot);   // MODE 0: X slice
+  uint16_t* bo = reinterpret_cast<uint16_t*>(slot);   // MODE 1: B-operand image
+  // Each wave owns its sparse output buffer (gather mode): within a wave the
+  // LDS unit applies adds in a fixed order, so repeated calls are identical.
+  float* shc_all = reinterpret_cast<float*>(smem + a.off_shc);
+  float* shc = shc_all + size_t(wave) * a.M * 64;
   int* flag = reinterpret_cast<int*>(smem + a.off_flag);
 
-  // ---------------------------------------------------------------- phase A
-  TileRegs cur;
-  if (DENSE && wave < nt) load_tile(a, t_lo + wave, n0, h, c4, cur);
+  if (SPARSE && MODE == 0)
+    for (int i = lane; i < a.M * 64; i += 64) shc[i] = 0.f;
+  if (SPARSE && MODE == 1) {
+    uint4* b4 = reinterpret_cast<uint4*>(bo);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) b4[i * 64 + lane] = uint4{0u, 0u, 0u, 0u};
+  }
 
-  const int chunks = nt * 16;
-  for (int i = tid; i < a.M * chunks; i += 256) {
-    const int m = i / chunks;
-    const int c = i - m * chunks;
-    const uint4 w = *reinterpret_cast<const uint4*>(a.X + size_t(m) * a.K + k0 + 8 * c);
-    *reinterpret_cast<uint4*>(Xs + m * a.xstride + 8 * c) = permute_chunk(w);
+  // Group offsets of this wave's tiles: lane i holds tile_indptr[w_lo + i].
+  uint32_t tp = 0;
+  if (SPARSE && lane <= w_hi - w_lo) {
+    const uint32_t v = a.tile_indptr[tile_base + w_lo + lane];
+    tp = uint32_t(min(int64_t(v), a.n_groups));
   }
-  if (SPARSE) {
-    for (int i = tid; i <= nt; i += 256) tptr[i] = a.tile_indptr[tile0 + i];
-    for (int i = tid; i < nt * a.B; i += 256) binfo[i] = a.bucket_info32[tile0 * a.B + i];
-    for (int i = tid; i < MR * 64; i += 256) shc[i] = 0.f;
-  }
-  __syncthreads();
+  __builtin_amdgcn_wave_barrier();
 
-  int64_t g_lo = 0, g_hi = 0;
-  bool staged = false;
-  if (SPARSE) {
-    g_lo = min(int64_t(tptr[0]), a.n_groups);
-    g_hi = max(g_lo, min(int64_t(tptr[nt]), a.n_groups));
-    staged = (g_hi - g_lo) <= a.stage_cap;
-    if (staged)
-      for (int64_t i = tid; i < g_hi - g_lo; i += 256) stage[i] = a.packed[g_lo + i];
-  }
-  if (DENSE) {
-    // Xsum[tile][row] = sum of the tile's 128 activations of that row, fp32.
-    for (int i = tid; i < nt * MR; i += 256) {
-      const int tl = i / MR;
-      const int m = i - tl * MR;
-      float s = 0.f;
-      if (m < a.M) {
-        const uint4* row = reinterpret_cast<const uint4*>(Xs + m * a.xstride + tl * 128);
-        for (int c = 0; c < 16; ++c) {
-          const uint4 w = row[c];
-          s += bf16_bits_to_f32(w.x & 0xFFFFu) + bf16_bits_to_f32(w.x >> 16);
-          s += bf16_bits_to_f32(w.y & 0xFFFFu) + bf16_bits_to_f32(w.y >> 16);
-          s += bf16_bits_to_f32(w.z & 0xFFFFu) + bf16_bits_to_f32(w.z >> 16);
-          s += bf16_bits_to_f32(w.w & 0xFFFFu) + bf16_bits_to_f32(w.w >> 16);
-        }
-      }
-      Xsum[i] = s;
-    }
-  }
-  __syncthreads();
-
-  // ------------------------------------------------------------ dense path
   f32x4_t acc[MB][4];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const bf16x8_t ones = __builtin_bit_cast(
+      bf16x8_t, u32x4_t{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
 
-  if (DENSE) {
-    for (int tl = wave; tl < nt; tl += 4) {
-      TileRegs nxt;
-      const bool more = tl + 4 < nt;
-      if (more) load_tile(a, t_lo + tl + 4, n0, h, c4, nxt);
+  auto issue = [&](int t, TileRegs<MB, MODE>& r) {
+    uint32_t g0 = 0, g1 = 0;
+    if (SPARSE) {
+      g0 = uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo));
+      g1 = max(g0, uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo + 1)));
+    }
+    load_tile<MB, MODE, DENSE, SPARSE>(a, t, n0, lane, g0, g1, r);
+  };
 
-      f32x4_t tmp[MB][4];
+  auto compute = [&](const TileRegs<MB, MODE>& cur) {
+    // ---- X fragments
+    bf16x8_t A[MB][4];
+    if (MODE == 0) {
+      // stage the slice (lanes past the last row rewrite row M-1 with the
+      // same values, which keeps the store unconditional), then read it back
+      // in MFMA operand order
+      const int m = min(lane >> 4, a.M - 1);
+      *reinterpret_cast<uint4*>(xs + m * XS + 8 * (lane & 15)) = permute_chunk(cur.x[0]);
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int step = 0; step < 4; ++step)
+        A[0][step] = *reinterpret_cast<const bf16x8_t*>(xs + min(c4, a.M - 1) * XS + step * 32 + 8 * h);
+    } else {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
+        for (int step = 0; step < 4; ++step)
+          A[mb][step] = __builtin_bit_cast(bf16x8_t, permute_chunk(cur.x[mb * 4 + step]));
+    }
+
+    // ---- scatter the tile's outliers (MFMA mode); overlaps the dense MFMAs
+    uint32_t n_g = 0;
+    if (SPARSE) n_g = cur.g1 - cur.g0;
+    if (SPARSE && MODE == 1) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        if (uint32_t(lane + 64 * j) < n_g) scatter_group(bo, cur.g[j], false);
+      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
+        scatter_group(bo, a.packed[cur.g0 + gi], false);
+      __builtin_amdgcn_wave_barrier();
+    }
+
+    // ---- dense path
+    if (DENSE) {
+      f32x4_t tmp[MB][4], xsum[MB];
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        xsum[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
         for (int c = 0; c < 4; ++c) tmp[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
 #pragma unroll
       for (int step = 0; step < 4; ++step) {
-        bf16x8_t A[MB];
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          const int m = mb * 16 + c4;
-          if (m < a.M) {
-            A[mb] = *reinterpret_cast<const bf16x8_t*>(Xs + m * a.xstride + tl * 128 + step * 32 + 8 * h);
-          } else {
-            A[mb] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
-          }
-        }
         const uint32_t w4[4] = {cur.w[step].x, cur.w[step].y, cur.w[step].z, cur.w[step].w};
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           const bf16x8_t Bq = dequant_word(w4[c]);
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
-            tmp[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb], Bq, tmp[mb][c], 0, 0, 0);
+            tmp[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bq, tmp[mb][c], 0, 0, 0);
         }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+          xsum[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], ones, xsum[mb], 0, 0, 0);
       }
-      // Group epilogue: acc += s * (sum x (16+q) - (16+z) * sum x).
-      float s[4], zf[4];
-      s[0] = f16_bits_to_f32(cur.s.x & 0xFFFFu);
-      s[1] = f16_bits_to_f32(cur.s.x >> 16);
-      s[2] = f16_bits_to_f32(cur.s.y & 0xFFFFu);
-      s[3] = f16_bits_to_f32(cur.s.y >> 16);
+      float sc[4], zf[4];
+      sc[0] = f16_bits_to_f32(cur.s.x & 0xFFFFu);
+      sc[1] = f16_bits_to_f32(cur.s.x >> 16);
+      sc[2] = f16_bits_to_f32(cur.s.y & 0xFFFFu);
+      sc[3] = f16_bits_to_f32(cur.s.y >> 16);
       const int zsh = (c4 & 1) * 16;
 #pragma unroll
       for (int c = 0; c < 4; ++c) zf[c] = 16.f + float((cur.z >> (zsh + 4 * c)) & 15u);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const f32x4_t xs = *reinterpret_cast<const f32x4_t*>(Xsum + tl * MR + mb * 16 + 4 * h);
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int c = 0; c < 4; ++c)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            acc[mb][c][r] += s[c] * (tmp[mb][c][r] - zf[c] * xs[r]);
-      }
-      if (more) cur = nxt;
+            acc[mb][c][r] += sc[c] * (tmp[mb][c][r] - zf[c] * xsum[mb][r]);
     }
-  }
 
-  // ----------------------------------------------------------- sparse path
-  if (SPARSE) {
-    const int B = a.B;
-    const int n_slots = 256 / B;
-    const int slot = tid / B;
-    const int b = tid - slot * B;
-    if (slot < n_slots) {
-      for (int tl = slot; tl < nt; tl += n_slots) {
-        const uint32_t info = binfo[tl * B + b];
-        const int64_t ts = max(int64_t(tptr[tl]), g_lo);
-        const int64_t te = max(ts, min(int64_t(tptr[tl + 1]), g_hi));
-        const int64_t gb = min(ts + int64_t(info & 0xFFFFu), te);
-        const int64_t ge = min(gb + int64_t(info >> 16), te);
-        const uint16_t* xt = Xs + tl * 128;
-        for (int64_t g = gb; g < ge; ++g) {
-          const Group d = decode_group(staged ? stage[g - g_lo] : a.packed[g]);
-          const uint32_t p4 = chunk_pos4(d.rows & 0x7F7F7F7Fu);
-          const uint32_t p0 = p4 & 0xFFu, p1 = (p4 >> 8) & 0xFFu;
-          const uint32_t p2 = (p4 >> 16) & 0xFFu, p3 = p4 >> 24;
-          if (single_column(d)) {
-            float* out = shc + (d.cols & 63u);
-            for (int m = 0; m < a.M; ++m) {
-              const uint16_t* xr = xt + m * a.xstride;
-              const uint32_t x01 = uint32_t(xr[p0]) | (uint32_t(xr[p1]) << 16);
-              const uint32_t x23 = uint32_t(xr[p2]) | (uint32_t(xr[p3]) << 16);
-              const float part = dot2_bf16(x23, d.v23, dot2_bf16(x01, d.v01, 0.f));
-              atomicAdd(out + m * 64, part);
-            }
-          } else {
-            const uint32_t pj[4] = {p0, p1, p2, p3};
-            for (int m = 0; m < a.M; ++m) {
-              const uint16_t* xr = xt + m * a.xstride;
+    // ---- sparse path
+    if (SPARSE && MODE == 1) {
+      const uint4* b4 = reinterpret_cast<const uint4*>(bo);
 #pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                const uint32_t v = slot_val(d, j);
-                if (v != 0u)
-                  atomicAdd(shc + m * 64 + (slot_col(d, j) & 63u),
-                            bf16_bits_to_f32(xr[pj[j]]) * bf16_bits_to_f32(v));
-              }
-            }
-          }
+      for (int step = 0; step < 4; ++step)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const bf16x8_t Bo = __builtin_bit_cast(bf16x8_t, b4[(step * 4 + c) * 64 + lane]);
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+            acc[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bo, acc[mb][c], 0, 0, 0);
         }
-      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        if (uint32_t(lane + 64 * j) < n_g) scatter_group(bo, cur.g[j], true);
+      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
+        scatter_group(bo, a.packed[cur.g0 + gi], true);
+    }
+    if (SPARSE && MODE == 0) {
+      // lane l takes groups l, l + 64, ...: the first two from the prefetch
+      // registers, any further ones straight from memory
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        if (uint32_t(lane + 64 * j) < n_g) sparse_gather(a, xs, cur.g[j], shc);
+      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
+        sparse_gather(a, xs, a.packed[cur.g0 + gi], shc);
+    }
+    __builtin_amdgcn_wave_barrier();
+  };
+
+  // Two register buffers, both in flight: while tile t is computed from one,
+  // the loads of tile t+1 fill the other; when t is done its buffer is
+  // refilled with tile t+2.  Every issue is unconditional (past the wave's
+  // last tile it re-reads that tile, which is still in cache), so the loop is
+  // straight-line and each wait is exact: waiting for tile t leaves the NL
+  // loads of the following tile in flight.
+  constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
+  TileRegs<MB, MODE> ra, rb;
+  if (w_lo < w_hi) {
+    const int last = w_hi - 1;
+    issue(w_lo, ra);
+    issue(min(w_lo + 1, last), rb);
+    for (int t = w_lo;;) {
+      wait_vmcnt<NL>();
+      compute(ra);
+      issue(min(t + 2, last), ra);
+      if (++t >= w_hi) break;
+      wait_vmcnt<NL>();
+      compute(rb);
+      issue(min(t + 2, last), rb);
+      if (++t >= w_hi) break;
     }
   }
   __syncthreads();
 
   // ---------------------------------------------------------------- reduce
-  if (DENSE) {
-    if (RED_SLOTS == 4) {
+  float* red = reinterpret_cast<float*>(smem);   // reuses the wave slots
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = mb * 16 + 4 * h + r;
-          *reinterpret_cast<f32x4_t*>(red + (wave * MR + row) * 64 + 4 * c4) =
-              f32x4_t{acc[mb][0][r], acc[mb][1][r], acc[mb][2][r], acc[mb][3][r]};
-        }
-    } else {
-      for (int w = 0; w < 4; ++w) {
-        if (wave == w) {
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int row = mb * 16 + 4 * h + r;
-              f32x4_t* dst = reinterpret_cast<f32x4_t*>(red + row * 64 + 4 * c4);
-              const f32x4_t v{acc[mb][0][r], acc[mb][1][r], acc[mb][2][r], acc[mb][3][r]};
-              *dst = (w == 0) ? v : (*dst + v);
-            }
-        }
-        __syncthreads();
-      }
+    for (int r = 0; r < 4; ++r) {
+      const int row = mb * 16 + 4 * h + r;
+      if (row < a.M)
+        *reinterpret_cast<f32x4_t*>(red + (wave * a.M + row) * 64 + 4 * c4) =
+            f32x4_t{acc[mb][0][r], acc[mb][1][r], acc[mb][2][r], acc[mb][3][r]};
     }
-  }
   __syncthreads();
 
   const bool split_k = a.S > 1;
@@ -320,37 +428,49 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
     const int m = i >> 4;
     const int cq = i & 15;
     f32x4_t v{0.f, 0.f, 0.f, 0.f};
-    if (DENSE) {
 #pragma unroll
-      for (int w = 0; w < RED_SLOTS; ++w)
-        v += *reinterpret_cast<const f32x4_t*>(red + (w * MR + m) * 64 + 4 * cq);
+    for (int w = 0; w < 4; ++w)
+      v += *reinterpret_cast<const f32x4_t*>(red + (w * a.M + m) * 64 + 4 * cq);
+    if (SPARSE && MODE == 0) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        v += *reinterpret_cast<const f32x4_t*>(shc_all + (w * a.M + m) * 64 + 4 * cq);
     }
-    if (SPARSE) v += *reinterpret_cast<const f32x4_t*>(shc + m * 64 + 4 * cq);
     if (split_k) {
-      *reinterpret_cast<f32x4_t*>(a.partials + ((size_t(strip) * a.S + split) * MR + m) * 64 + 4 * cq) = v;
+      // Partial sums travel through device-coherent (agent-scope) stores and
+      // loads, so no cache-wide writeback or invalidate is needed.
+      float* dst = a.partials + ((size_t(strip) * a.S + split) * a.M + m) * 64 + 4 * cq;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        __hip_atomic_store(dst + j, v[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     } else {
       store_out(a, m, n0 + 4 * cq, v);
     }
   }
   if (split_k) {
-    __threadfence();
+    __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores have completed
     __syncthreads();
     if (tid == 0) {
-      const uint32_t old = atomicAdd(a.counters + strip, 1u);
+      const uint32_t old =
+          __hip_atomic_fetch_add(a.counters + strip, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       *flag = (old == uint32_t(a.S - 1));
     }
     __syncthreads();
     if (*flag) {
-      __threadfence();
       for (int i = tid; i < a.M * 16; i += 256) {
         const int m = i >> 4;
         const int cq = i & 15;
         f32x4_t v{0.f, 0.f, 0.f, 0.f};
-        for (int sp = 0; sp < a.S; ++sp)
-          v += *reinterpret_cast<const f32x4_t*>(a.partials + ((size_t(strip) * a.S + sp) * MR + m) * 64 + 4 * cq);
+        for (int sp = 0; sp < a.S; ++sp) {
+          const float* src = a.partials + ((size_t(strip) * a.S + sp) * a.M + m) * 64 + 4 * cq;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            v[j] += __hip_atomic_load(src + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         store_out(a, m, n0 + 4 * cq, v);
       }
-      if (tid == 0) a.counters[strip] = 0u;
+      if (tid == 0)
+        __hip_atomic_store(a.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -380,9 +500,9 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
   }
 }
 
-template <int MB, bool DENSE, bool SPARSE>
+template <int MB, int MODE, bool DENSE, bool SPARSE>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, DENSE, SPARSE>;
+  auto kern = matmul_kernel<MB, MODE, DENSE, SPARSE>;
   if (pl.lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -394,64 +514,64 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
   return int(hipGetLastError());
 }
 
+template <int MB, int MODE>
+int launch_mode(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
+  if (dense && sparse) return launch_variant<MB, MODE, true, true>(pl, a, s);
+  if (dense) return launch_variant<MB, MODE, true, false>(pl, a, s);
+  return launch_variant<MB, MODE, false, true>(pl, a, s);
+}
+
 }  // namespace fqk
 
 namespace fqi {
 
 namespace {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int default_split(int T, int n_strips) {
+  // About 256 workgroups (one per CU, four waves each), at least one tile
+  // per wave; wide matrices need no split at all.
+  int S = (256 + n_strips - 1) / n_strips;
+  S = std::min(S, std::max(1, T / 4));
+  return std::max(S, 1);
+}
 }  // namespace
 
 bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
-               int64_t max_tile_groups, Plan* pl) {
+               int64_t max_tile_groups, Plan* pl, int mode) {
+  (void)max_tile_groups;
   if (M < 1 || M > kMaxM || K < kTileK || N < kTileN || K % kTileK || N % kTileN) return false;
+  if (N / kTileN > kMaxStrips) return false;
   if (sparse && (B < 1 || B > kMaxBuckets)) return false;
   Plan p{};
   p.M = M;
   p.K = K;
   p.N = N;
   p.MB = M <= 16 ? 1 : 2;
-  const int MR = 16 * p.MB;
+  p.MODE = mode >= 0 ? mode : (M <= kGatherMaxM ? 0 : 1);
+  if (p.MODE == 0 && M > 16) return false;   // gathers use one 16-row block
   p.n_strips = N / kTileN;
   p.T = K / kTileK;
-  // Activations staged per workgroup: keep them within 32 KiB of LDS.
-  const int nt_cap = std::max(1, (32768 / (2 * M) - 8) / kTileK);
-  int S;
-  if (split_k > 0) {
-    S = std::min(split_k, p.T);
-  } else {
-    const int s_lds = (p.T + nt_cap - 1) / nt_cap;
-    const int s_par = (1024 + p.n_strips - 1) / p.n_strips;
-    S = std::min(std::max(s_lds, s_par), std::max(s_lds, p.T / 4));
-    S = std::max(1, std::min(S, p.T));
-  }
-  p.S = S;
-  p.nt_max = (p.T + S - 1) / S;
-  p.xstride = p.nt_max * kTileK + 8;
-  p.B = sparse ? B : 0;
-  const int64_t want = sparse ? max_tile_groups * p.nt_max : 0;
-  p.stage_cap = int(std::min<int64_t>(want, 1024));
+  int S = split_k > 0 ? split_k : default_split(p.T, p.n_strips);
+  // each wave indexes its tiles' group offsets from one register: <= 63 tiles
+  S = std::max(S, (p.T + 4 * 63 - 1) / (4 * 63));
+  p.S = std::max(1, std::min(S, p.T));
+  p.B = sparse ? B : 1;
 
-  const size_t x_bytes = size_t(M) * p.xstride * 2;
-  const size_t red_bytes = dense ? size_t(p.MB <= 2 ? 4 : 1) * MR * kTileN * 4 : 0;
-  size_t off = align_up(std::max(x_bytes, red_bytes), 16);
-  p.off_xsum = off;
-  off = align_up(off + size_t(p.nt_max) * MR * 4, 16);
-  p.off_shc = off;
-  off = align_up(off + (sparse ? size_t(MR) * kTileN * 4 : 0), 16);
-  p.off_stage = off;
-  off = align_up(off + size_t(p.stage_cap) * 16, 16);
-  p.off_binfo = off;
-  off = align_up(off + (sparse ? size_t(p.nt_max) * p.B * 4 : 0), 16);
-  p.off_tptr = off;
-  off = align_up(off + size_t(p.nt_max + 1) * 4, 16);
-  p.off_flag = off;
-  p.lds_bytes = align_up(off + 16, 16);
+  if (p.MODE == 0) {
+    p.slot_bytes = align_up(size_t(M) * kXStride * 2, 16);
+  } else {
+    p.slot_bytes = sparse ? size_t(16) * 64 * 16 : 0;   // 16 B-operand blocks of 64 x 16 B
+  }
+  const size_t red_bytes = size_t(4) * M * kTileN * 4;
+  p.off_shc = align_up(std::max(4 * p.slot_bytes, red_bytes), 16);
+  const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(4) * M * kTileN * 4 : 0;
+  p.off_flag = align_up(p.off_shc + shc_bytes, 16);
+  p.lds_bytes = p.off_flag + 16;
   if (p.lds_bytes > 160 * 1024) return false;
 
-  p.partial_bytes = S > 1 ? size_t(p.n_strips) * S * MR * kTileN * 4 : 0;
-  p.counter_offset = align_up(p.partial_bytes, 256);
-  p.ws_bytes = p.counter_offset + align_up(size_t(p.n_strips) * 4, 256);
+  p.partial_bytes = p.S > 1 ? size_t(p.n_strips) * p.S * M * kTileN * 4 : 0;
+  p.ws_bytes = kCounterRegion + align_up(p.partial_bytes, 256);
   *pl = p;
   return true;
 }
@@ -463,37 +583,32 @@ int launch_matmul(const Plan& pl, const MatmulPtrs& p, bool dense, bool sparse, 
   a.scales = p.scales;
   a.zeros = p.zeros;
   a.tile_indptr = p.tile_indptr;
-  a.bucket_info32 = reinterpret_cast<const uint32_t*>(p.bucket_info);
   a.packed = reinterpret_cast<const uint4*>(p.packed);
   a.n_groups = p.n_groups;
   a.y_addend = p.y_addend;
   a.Y = p.Y;
   a.y_f32 = p.y_f32;
-  a.partials = static_cast<float*>(p.workspace);
-  a.counters = reinterpret_cast<uint32_t*>(static_cast<char*>(p.workspace) + pl.counter_offset);
+  a.counters = static_cast<uint32_t*>(p.workspace);
+  a.partials = reinterpret_cast<float*>(static_cast<char*>(p.workspace) + kCounterRegion);
   a.M = pl.M;
   a.K = pl.K;
   a.N = pl.N;
   a.T = pl.T;
   a.S = pl.S;
-  a.xstride = pl.xstride;
-  a.B = sparse ? pl.B : 1;
-  a.stage_cap = pl.stage_cap;
-  a.off_xsum = int(pl.off_xsum);
+  a.slot_bytes = int(pl.slot_bytes);
   a.off_shc = int(pl.off_shc);
-  a.off_stage = int(pl.off_stage);
-  a.off_binfo = int(pl.off_binfo);
-  a.off_tptr = int(pl.off_tptr);
   a.off_flag = int(pl.off_flag);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (pl.MB == 1) {
-    if (dense && sparse) return fqk::launch_variant<1, true, true>(pl, a, s);
-    if (dense) return fqk::launch_variant<1, true, false>(pl, a, s);
-    return fqk::launch_variant<1, false, true>(pl, a, s);
+  if (sparse && p.n_groups == 0) {
+    // No outliers: the fused launch drops its sparse half; a sparse-only
+    // launch still writes Y (= y_addend) and reads its always-empty group
+    // ranges from the workspace, which is valid device memory.
+    if (dense) sparse = false;
+    else a.packed = reinterpret_cast<const uint4*>(p.workspace);
   }
-  if (dense && sparse) return fqk::launch_variant<2, true, true>(pl, a, s);
-  if (dense) return fqk::launch_variant<2, true, false>(pl, a, s);
-  return fqk::launch_variant<2, false, true>(pl, a, s);
+  if (pl.MODE == 0) return fqk::launch_mode<1, 0>(pl, a, dense, sparse, s);
+  if (pl.MB == 1) return fqk::launch_mode<1, 1>(pl, a, dense, sparse, s);
+  return fqk::launch_mode<2, 1>(pl, a, dense, sparse, s);
 }
 
 int launch_decode(const uint32_t* tile_indptr, int64_t n_tiles, const uint32_t* packed,

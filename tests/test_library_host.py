@@ -236,7 +236,7 @@ def test_storage_formula_on_library_output(lib):
 # Only argument checks that fail before any launch are exercised here.
 
 def _problem(**kw):
-    d = dict(M=4, K=1024, N=512, group_size=128, y_dtype=0, split_k=0)
+    d = dict(M=4, K=1024, N=512, group_size=128, y_dtype=0, split_k=0, flags=0)
     d.update(kw)
     return fq.fq_problem(**d)
 
@@ -268,6 +268,8 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
     (dict(group_size=64), "FQ_ERR_UNSUPPORTED"),
     (dict(y_dtype=5), "FQ_ERR_UNSUPPORTED"),
     (dict(split_k=-1), "FQ_ERR_SHAPE"),
+    (dict(flags=3), "FQ_ERR_UNSUPPORTED"),
+    (dict(flags=1, M=17), "FQ_ERR_UNSUPPORTED"),
 ])
 def test_matmul_rejects_bad_problem(lib, kw, status):
     assert _call(lib, _problem(**kw)) == status
