@@ -192,8 +192,8 @@ typedef struct {
   int32_t flags;
 } fq_problem;
 
-/* Sparse-path mappings (fq_problem.flags).  GATHER: each lane decodes one
- * 16-byte group and gathers X[m][k] from LDS for every row (VALU dot2).
+/* Sparse-path mappings (fq_problem.flags).  GATHER (M <= 4 only): each lane
+ * decodes one 16-byte group and gathers X[m][k] from LDS for every row (VALU dot2).
  * MFMA: the tile's outliers are scattered into an LDS image of the MFMA B
  * operand and multiplied on the matrix cores.  Both are exact in fp32. */
 enum { FQ_SPARSE_AUTO = 0, FQ_SPARSE_GATHER = 1, FQ_SPARSE_MFMA = 2 };

@@ -17,7 +17,7 @@ fq_status check_problem(const fq_problem* pr) {
   if (pr->M > fqi::kMaxM) return FQ_ERR_UNSUPPORTED;
   if (pr->y_dtype != FQ_Y_BF16 && pr->y_dtype != FQ_Y_F32) return FQ_ERR_UNSUPPORTED;
   if (pr->flags < FQ_SPARSE_AUTO || pr->flags > FQ_SPARSE_MFMA) return FQ_ERR_UNSUPPORTED;
-  if (pr->flags == FQ_SPARSE_GATHER && pr->M > 16) return FQ_ERR_UNSUPPORTED;
+  if (pr->flags == FQ_SPARSE_GATHER && pr->M > fqi::kGatherLimitM) return FQ_ERR_UNSUPPORTED;
   return FQ_OK;
 }
 

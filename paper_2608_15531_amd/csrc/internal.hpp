@@ -13,7 +13,8 @@ constexpr int kThreads = 256;   // four wave64 per workgroup
 constexpr int kMaxM = 32;       // rows the fused GEMV-regime kernel supports
 constexpr int kMaxBuckets = 256;
 constexpr int kXStride = 136;   // LDS row stride (elements) of a staged 128-wide X slice
-constexpr int kGatherMaxM = 4;  // up to this M the sparse path gathers X in LDS; above, MFMA
+constexpr int kGatherMaxM = 3;  // up to this M the sparse path gathers X in LDS; above, MFMA
+constexpr int kGatherLimitM = 4; // rows the gather mapping can stage at all
 // The workspace starts with a fixed counter region (one uint32 per 64-column
 // strip, zero between calls) so that a workspace shared by problems of
 // different shapes never finds partial sums where a counter is expected.

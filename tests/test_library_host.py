@@ -269,7 +269,7 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
     (dict(y_dtype=5), "FQ_ERR_UNSUPPORTED"),
     (dict(split_k=-1), "FQ_ERR_SHAPE"),
     (dict(flags=3), "FQ_ERR_UNSUPPORTED"),
-    (dict(flags=1, M=17), "FQ_ERR_UNSUPPORTED"),
+    (dict(flags=1, M=5), "FQ_ERR_UNSUPPORTED"),
 ])
 def test_matmul_rejects_bad_problem(lib, kw, status):
     assert _call(lib, _problem(**kw)) == status
