@@ -174,8 +174,13 @@ typedef struct {
 
 /*
  * Problem description for the device entry points.
- *   M           rows of X and Y, 1..128.
- *   K, N        K % 128 == 0, N % 64 == 0.
+ *   M           rows of X and Y, >= 1; the kernels implement 1..32
+ *               (FQ_ERR_UNSUPPORTED above).
+ *   K, N        K % 128 == 0, N % 64 == 0.  The kernels address every array
+ *               with 32-bit byte offsets: Wq (K N / 2 bytes), X (2 M K bytes),
+ *               the split-K partial sums (4 M N split_k bytes) and the packed
+ *               Tile-COO groups (16 n_groups bytes) must each stay below 2^31
+ *               bytes, else FQ_ERR_UNSUPPORTED.
  *   group_size  G, must be 128 (one group per 128 x 64 tile).
  *   y_dtype     FQ_Y_BF16 (round to nearest even once, after the full sum) or FQ_Y_F32.
  *   split_k     number of K ranges per 64-column strip; 0 lets the library choose.

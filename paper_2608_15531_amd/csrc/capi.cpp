@@ -36,8 +36,8 @@ fq_status check_tc(const fq_problem* pr, const fq_tilecoo_dev* tc) {
   if (p.k_tile != fqi::kTileK || p.n_tile != fqi::kTileN) return FQ_ERR_UNSUPPORTED;
   if (p.buckets_per_tile < 1 || p.buckets_per_tile > fqi::kMaxBuckets) return FQ_ERR_UNSUPPORTED;
   if (p.group_mode != FQ_GROUP_BY_COLUMN && p.group_mode != FQ_GROUP_BY_BUCKET) return FQ_ERR_FORMAT;
-  if (tc->n_groups < 0 || tc->max_tile_groups < 0 || tc->n_groups > 0xFFFFFFFFll)
-    return FQ_ERR_FORMAT;
+  if (tc->n_groups < 0 || tc->max_tile_groups < 0) return FQ_ERR_FORMAT;
+  if (tc->n_groups >= (int64_t(1) << 27)) return FQ_ERR_UNSUPPORTED;   // 16-byte groups < 2^31 B
   if (!tc->tile_indptr || !tc->bucket_info || (tc->n_groups > 0 && !tc->packed)) return FQ_ERR_NULL;
   if (!aligned(tc->tile_indptr, 4) || !aligned(tc->bucket_info, 4) || !aligned(tc->packed, 16))
     return FQ_ERR_ALIGN;

@@ -26,13 +26,20 @@ typedef uint32_t u32x4_t __attribute__((__vector_size__(4 * sizeof(uint32_t))));
 // so (q - z) never needs to be formed and the scale s is applied in fp32 once
 // per group (eq. 3 of the paper).
 // ---------------------------------------------------------------------------
+// (a & b) | c as one VALU operation (gfx950 three-input bitwise op; truth
+// table 0xEA).  Plain C++ for this pattern compiles to two VOP2 operations,
+// because a VOP3 encoding cannot carry the two literal constants.
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0xEA);
+}
+
 __device__ __forceinline__ bf16x8_t dequant_word(uint32_t w) {
   const uint32_t mask = 0x00780078u, bias = 0x41804180u;
   u32x4_t r;
-  r[0] = ((w << 3) & mask) | bias;
-  r[1] = ((w >> 1) & mask) | bias;
-  r[2] = ((w >> 5) & mask) | bias;
-  r[3] = ((w >> 9) & mask) | bias;
+  r[0] = and_or(w << 3, mask, bias);
+  r[1] = and_or(w >> 1, mask, bias);
+  r[2] = and_or(w >> 5, mask, bias);
+  r[3] = and_or(w >> 9, mask, bias);
   return __builtin_bit_cast(bf16x8_t, r);
 }
 
@@ -47,13 +54,14 @@ __device__ __forceinline__ uint32_t chunk_pos4(uint32_t k4) {
   return (k4 & 0xF8F8F8F8u) | ((k4 & 0x03030303u) << 1) | ((k4 >> 2) & 0x01010101u);
 }
 
-// 16 bytes of X (x0..x7) -> chunk order (x0,x4,x1,x5,x2,x6,x3,x7).
+// 16 bytes of X (x0..x7) -> chunk order (x0,x4,x1,x5,x2,x6,x3,x7): one byte
+// permute per output dword.
 __device__ __forceinline__ uint4 permute_chunk(uint4 w) {
   uint4 o;
-  o.x = (w.x & 0xFFFFu) | (w.z << 16);
-  o.y = (w.x >> 16) | (w.z & 0xFFFF0000u);
-  o.z = (w.y & 0xFFFFu) | (w.w << 16);
-  o.w = (w.y >> 16) | (w.w & 0xFFFF0000u);
+  o.x = __builtin_amdgcn_perm(w.z, w.x, 0x05040100u);   // x0 | x4 << 16
+  o.y = __builtin_amdgcn_perm(w.z, w.x, 0x07060302u);   // x1 | x5 << 16
+  o.z = __builtin_amdgcn_perm(w.w, w.y, 0x05040100u);   // x2 | x6 << 16
+  o.w = __builtin_amdgcn_perm(w.w, w.y, 0x07060302u);   // x3 | x7 << 16
   return o;
 }
 

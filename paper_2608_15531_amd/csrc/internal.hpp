@@ -15,6 +15,7 @@ constexpr int kMaxBuckets = 256;
 constexpr int kXStride = 136;   // LDS row stride (elements) of a staged 128-wide X slice
 constexpr int kGatherMaxM = 3;  // up to this M the sparse path gathers X in LDS; above, MFMA
 constexpr int kGatherLimitM = 4; // rows the gather mapping can stage at all
+constexpr int kImageBytes = 16384;   // one wave's B-operand image of a 128 x 64 tile
 // The workspace starts with a fixed counter region (one uint32 per 64-column
 // strip, zero between calls) so that a workspace shared by problems of
 // different shapes never finds partial sums where a counter is expected.
@@ -34,7 +35,7 @@ struct Plan {
   int B;             // buckets per tile
   // dynamic LDS layout, bytes: four wave slots (X slice or B-operand image),
   // then the gather-mode sparse output buffers
-  size_t slot_bytes, off_shc, off_flag, lds_bytes;
+  size_t slot_bytes, off_shc, off_flag, off_trash, lds_bytes;
   // workspace layout, bytes: counters at 0, partial sums at kCounterRegion
   size_t partial_bytes, ws_bytes;
 };

@@ -43,6 +43,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "device.hpp"
 #include "internal.hpp"
@@ -69,6 +70,7 @@ struct MatmulArgs {
   int slot_bytes;      // one wave's LDS slot
   int off_shc;         // per-wave sparse output buffers (gather mode)
   int off_flag;
+  int off_trash;       // 16 bytes that padding slots are written to (MFMA mode)
 };
 
 // Global loads one tile costs in each mode (each counts once in vmcnt).
@@ -76,6 +78,14 @@ template <int MB, int MODE, bool DENSE, bool SPARSE>
 constexpr int loads_per_tile() {
   return (DENSE ? 6 : 0) + (MODE == 0 ? 1 : 4 * MB) + (SPARSE ? 2 : 0);
 }
+
+#ifndef FQ_PIPELINE_DEPTH
+#define FQ_PIPELINE_DEPTH 2
+#endif
+// Tiles in flight per wave.  Two 16-row blocks need twice the activation
+// registers, which leaves room for two buffers only.
+template <int MB>
+constexpr int pipeline_depth() { return MB == 1 ? FQ_PIPELINE_DEPTH : 2; }
 
 // Everything one wave needs for one tile, held in registers until used.
 template <int MB, int MODE>
@@ -90,44 +100,86 @@ struct TileRegs {
   uint32_t g0, g1; // the tile's group range
 };
 
-template <int MB, int MODE, bool DENSE, bool SPARSE>
-__device__ __forceinline__ void load_tile(const MatmulArgs& a, int t, int n0, int lane,
-                                          uint32_t g0, uint32_t g1, TileRegs<MB, MODE>& r) {
-  // Every load is unconditional (addresses clamped into range) so the
-  // compiler counts outstanding loads exactly across the prefetch.
-  const int h = lane >> 4;
-  const int c4 = lane & 15;
+// Every operand is read with raw buffer loads: a resource descriptor per
+// array (base and byte size, wave-uniform), a per-lane byte offset fixed for
+// the whole kernel, and a wave-uniform byte offset that moves from tile to
+// tile.  Address arithmetic therefore stays in scalar registers; the plan
+// keeps every array below 2^31 bytes.
+constexpr int kBufferWord3 = 0x00020000;   // raw 32-bit elements, no swizzle (gfx9)
+constexpr int kSc1 = 16;                   // cache-policy operand: device (agent) scope
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, int(bytes), kBufferWord3);
+}
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, int(voff), int(soff), 0));
+}
+__device__ __forceinline__ uint2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, int(voff), int(soff), 0));
+}
+__device__ __forceinline__ uint32_t buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, int(voff), int(soff), 0);
+}
+
+template <int MB>
+struct Operands {
+  __amdgpu_buffer_rsrc_t w, s, z, x, g;
+  uint32_t lw;       // Wq: row h of a 16-row step block, columns n0 + 4*c4 .. +3
+  uint32_t ls;       // scales of those columns
+  uint32_t lz;       // zero-point word holding them
+  uint32_t lx[MB];   // X: MODE 0 chunk lane; MODE 1 row 16mb + c4, elements 8h..
+};
+
+// The loads of a tile that do not depend on the Tile-COO offsets: packed
+// codes, scales and zero-points (dense path) and the tile's slice of X.
+// Every load is unconditional (offsets clamped into range) so the compiler
+// counts outstanding loads exactly across the prefetch.
+template <int MB, int MODE, bool DENSE>
+__device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Operands<MB>& op,
+                                                int t, int n0, TileRegs<MB, MODE>& r) {
   if (DENSE) {
-    const uint32_t* base = a.Wq + size_t(t * 16 + h) * a.N + n0 + 4 * c4;
+    const uint32_t step_bytes = uint32_t(a.N) * 16u;   // 4 rows of packed words = 32 k
+    const uint32_t wt = (uint32_t(t) * 16u * uint32_t(a.N) + uint32_t(n0)) * 4u;
 #pragma unroll
-    for (int step = 0; step < 4; ++step)
-      r.w[step] = *reinterpret_cast<const uint4*>(base + size_t(4 * step) * a.N);
-    r.s = *reinterpret_cast<const uint2*>(a.scales + size_t(t) * a.N + n0 + 4 * c4);
-    r.z = a.zeros[size_t(t) * (a.N >> 3) + ((n0 + 4 * c4) >> 3)];
+    for (int step = 0; step < 4; ++step) r.w[step] = buf_load16(op.w, op.lw, wt + step * step_bytes);
+    r.s = buf_load8(op.s, op.ls, (uint32_t(t) * uint32_t(a.N) + uint32_t(n0)) * 2u);
+    r.z = buf_load4(op.z, op.lz, (uint32_t(t) * uint32_t(a.N >> 3) + uint32_t(n0 >> 3)) * 4u);
   }
+  const uint32_t xt = uint32_t(t) * 256u;
   if (MODE == 0) {
-    const int m = min(lane >> 4, a.M - 1);
-    r.x[0] = *reinterpret_cast<const uint4*>(a.X + size_t(m) * a.K + t * 128 + 8 * (lane & 15));
+    r.x[0] = buf_load16(op.x, op.lx[0], xt);
   } else {
-    // Rows past M load row M-1; their output rows are never stored.
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int m = min(mb * 16 + c4, a.M - 1);
-      const uint16_t* row = a.X + size_t(m) * a.K + t * 128 + 8 * h;
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int step = 0; step < 4; ++step)
-        r.x[mb * 4 + step] = *reinterpret_cast<const uint4*>(row + 32 * step);
-    }
+      for (int step = 0; step < 4; ++step) r.x[mb * 4 + step] = buf_load16(op.x, op.lx[mb] + 64 * step, xt);
   }
+}
+
+// The tile's first two Tile-COO groups, one per lane and half-wave pass.
+template <int MB, int MODE, bool SPARSE>
+__device__ __forceinline__ void load_tile_sparse(const Operands<MB>& op, int lane, uint32_t g0,
+                                                 uint32_t g1, TileRegs<MB, MODE>& r) {
   if (SPARSE) {
     r.g0 = g0;
     r.g1 = g1;
     // Lanes past the tile's last group reload that group (same cache line),
     // never another tile's.  An empty tile reads group g0, which is in range:
     // with no outliers at all `packed` points at valid scratch.
-    const uint32_t last = g1 > g0 ? g1 - 1 : g0;
+    const uint32_t last = g1 > g0 ? g1 - 1 - g0 : 0u;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) r.g[j] = a.packed[min(g0 + uint32_t(lane + 64 * j), last)];
+    for (int j = 0; j < 2; ++j)
+      r.g[j] = buf_load16(op.g, min(uint32_t(lane + 64 * j), last) * 16u, g0 * 16u);
+  }
+}
+
+// Calls f(integral_constant<int, I>) for I = B .. E-1, in order.
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
   }
 }
 
@@ -195,22 +247,51 @@ __device__ __forceinline__ void sparse_gather(const MatmulArgs& a, const uint16_
   }
 }
 
-// MFMA mode: write (or clear) a group's real values into the wave's B-operand
-// image of the tile.  Element (k, n) of the tile lives where lane
-// (n/4 + 16 * ((k%32)/8)) reads B of MFMA (step k/32, column block n%4), at
-// the element the X fragment holds k at (chunk order x0,x4,x1,x5,...).
-__device__ __forceinline__ void scatter_group(uint16_t* bo, uint4 raw, bool clear) {
-  const Group d = decode_group(raw);
+// MFMA mode: the B-operand image of a tile.  Element (k, n) of the tile is
+// read by lane (n/4 + 16 * ((k%32)/8)) as B of MFMA (step k/32, column block
+// n%4), at the position its X partner holds k (chunk order x0,x4,x1,x5,...).
+// As a bf16 index into the wave's 16 KB image its bits are
+//   0: k2 | 1-2: k0,k1 | 3-6: n2..n5 | 7-8: k3,k4 | 9-10: n0,n1 | 11-12: k5,k6.
+// image_offsets forms the four byte offsets of a group at once, one slot per
+// byte lane while the index is split into its low and high bytes, then two
+// slots per dword (16-bit halves), with the slot's base folded in (the four
+// wave images fill the first 64 KB of LDS, so every offset fits 16 bits).
+__device__ __forceinline__ void image_offsets(uint32_t R, uint32_t C, uint32_t base2,
+                                              uint32_t& o01, uint32_t& o23) {
+  const uint32_t r1 = R << 1, r2 = R >> 2, c1 = C << 1;
+  uint32_t lo = r2 & 0x01010101u;               // k2
+  lo = and_or(r1, 0x06060606u, lo);             // k0, k1
+  lo = and_or(c1, 0x78787878u, lo);             // n2..n5
+  lo = and_or(R << 4, 0x80808080u, lo);         // k3
+  uint32_t hi = (R >> 4) & 0x01010101u;         // k4
+  hi = and_or(c1, 0x06060606u, hi);             // n0, n1
+  hi = and_or(r2, 0x18181818u, hi);             // k5, k6
+  // [lo0 hi0 lo1 hi1] and [lo2 hi2 lo3 hi3]: indices < 2^13, so doubling and
+  // adding the base never carries across the halves
+  o01 = (__builtin_amdgcn_perm(hi, lo, 0x05010400u) << 1) + base2;
+  o23 = (__builtin_amdgcn_perm(hi, lo, 0x07030602u) << 1) + base2;
+}
+
+// Writes a group's four values into the image and returns where they went:
+// a padding slot (value bits 0) goes to the trash word instead, since its
+// position may coincide with a real element of another group.
+__device__ __forceinline__ void scatter_group(unsigned char* smem, uint32_t base2, uint32_t trash,
+                                              uint4 raw, uint32_t addr[4]) {
+  uint32_t o01, o23;
+  image_offsets(raw.x, raw.y, base2, o01, o23);
+  addr[0] = (raw.z & 0xFFFFu) != 0u ? (o01 & 0xFFFFu) : trash;
+  addr[1] = raw.z > 0xFFFFu ? (o01 >> 16) : trash;
+  addr[2] = (raw.w & 0xFFFFu) != 0u ? (o23 & 0xFFFFu) : trash;
+  addr[3] = raw.w > 0xFFFFu ? (o23 >> 16) : trash;
+  *reinterpret_cast<uint16_t*>(smem + addr[0]) = uint16_t(raw.z);
+  *reinterpret_cast<uint16_t*>(smem + addr[1]) = uint16_t(raw.z >> 16);
+  *reinterpret_cast<uint16_t*>(smem + addr[2]) = uint16_t(raw.w);
+  *reinterpret_cast<uint16_t*>(smem + addr[3]) = uint16_t(raw.w >> 16);
+}
+
+__device__ __forceinline__ void clear_group(unsigned char* smem, const uint32_t addr[4]) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t v = slot_val(d, j);
-    if (v == 0u) continue;   // padding slots may share a real slot's position
-    const uint32_t k = slot_row(d, j) & 127u;
-    const uint32_t n = slot_col(d, j) & 63u;
-    const uint32_t lane = (n >> 2) + 16u * ((k >> 3) & 3u);
-    const uint32_t blk = (k >> 5) * 4u + (n & 3u);
-    bo[(blk * 64u + lane) * 8u + chunk_pos(k & 7u)] = clear ? uint16_t(0) : uint16_t(v);
-  }
+  for (int j = 0; j < 4; ++j) *reinterpret_cast<uint16_t*>(smem + addr[j]) = 0;
 }
 
 template <int MB, int MODE, bool DENSE, bool SPARSE>
@@ -242,6 +323,7 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
   unsigned char* slot = smem + size_t(wave) * a.slot_bytes;
   uint16_t* xs = reinterpret_cast<uint16_t*>(slot);   // MODE 0: X slice
   uint16_t* bo = reinterpret_cast<uint16_t*>(slot);   // MODE 1: B-operand image
+  static_assert(MODE != 1 || !SPARSE || fqi::kImageBytes == 16384, "image layout");
   // Each wave owns its sparse output buffer (gather mode): within a wave the
   // LDS unit applies adds in a fixed order, so repeated calls are identical.
   float* shc_all = reinterpret_cast<float*>(smem + a.off_shc);
@@ -257,11 +339,10 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
   }
 
   // Group offsets of this wave's tiles: lane i holds tile_indptr[w_lo + i].
+  // The value is used raw (clamped only when read) so that nothing waits for
+  // it before the first tiles' dense loads are out.
   uint32_t tp = 0;
-  if (SPARSE && lane <= w_hi - w_lo) {
-    const uint32_t v = a.tile_indptr[tile_base + w_lo + lane];
-    tp = uint32_t(min(int64_t(v), a.n_groups));
-  }
+  if (SPARSE && lane <= w_hi - w_lo) tp = a.tile_indptr[tile_base + w_lo + lane];
   __builtin_amdgcn_wave_barrier();
 
   f32x4_t acc[MB][4];
@@ -272,16 +353,42 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
   const bf16x8_t ones = __builtin_bit_cast(
       bf16x8_t, u32x4_t{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
 
-  auto issue = [&](int t, TileRegs<MB, MODE>& r) {
+  Operands<MB> op;
+  op.w = make_rsrc(a.Wq, uint32_t(a.K / 8) * uint32_t(a.N) * 4u);
+  op.s = make_rsrc(a.scales, uint32_t(a.K / 128) * uint32_t(a.N) * 2u);
+  op.z = make_rsrc(a.zeros, uint32_t(a.K / 128) * uint32_t(a.N / 8) * 4u);
+  op.x = make_rsrc(a.X, uint32_t(a.M) * uint32_t(a.K) * 2u);
+  op.g = make_rsrc(a.packed, uint32_t(max(a.n_groups, int64_t(1))) * 16u);
+  op.lw = uint32_t(h * a.N + 4 * c4) * 4u;
+  op.ls = uint32_t(c4) * 8u;
+  op.lz = uint32_t(c4 >> 1) * 4u;
+  if (MODE == 0) {
+    // rows past M load row M-1 (the slice store below is then a rewrite)
+    op.lx[0] = (uint32_t(min(lane >> 4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(lane & 15)) * 2u;
+  } else {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)   // rows past M load row M-1, never stored
+      op.lx[mb] = (uint32_t(min(mb * 16 + c4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(h)) * 2u;
+  }
+  const uint32_t img_base = uint32_t(wave) * uint32_t(a.slot_bytes);
+  const uint32_t img_base2 = img_base | (img_base << 16);
+  const uint32_t trash = uint32_t(a.off_trash);
+
+  auto issue_sparse = [&](int t, TileRegs<MB, MODE>& r) __attribute__((always_inline)) {
     uint32_t g0 = 0, g1 = 0;
     if (SPARSE) {
-      g0 = uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo));
-      g1 = max(g0, uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo + 1)));
+      const uint32_t ng = uint32_t(a.n_groups);   // < 2^27, checked on the host
+      g0 = min(uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo)), ng);
+      g1 = max(g0, min(uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo + 1)), ng));
     }
-    load_tile<MB, MODE, DENSE, SPARSE>(a, t, n0, lane, g0, g1, r);
+    load_tile_sparse<MB, MODE, SPARSE>(op, lane, g0, g1, r);
+  };
+  auto issue = [&](int t, TileRegs<MB, MODE>& r) __attribute__((always_inline)) {
+    load_tile_dense<MB, MODE, DENSE>(a, op, t, n0, r);
+    issue_sparse(t, r);
   };
 
-  auto compute = [&](const TileRegs<MB, MODE>& cur) {
+  auto compute = [&](const TileRegs<MB, MODE>& cur) __attribute__((always_inline)) {
     // ---- X fragments
     bf16x8_t A[MB][4];
     if (MODE == 0) {
@@ -305,12 +412,15 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
     // ---- scatter the tile's outliers (MFMA mode); overlaps the dense MFMAs
     uint32_t n_g = 0;
     if (SPARSE) n_g = cur.g1 - cur.g0;
+    uint32_t addr[2][4];
     if (SPARSE && MODE == 1) {
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        if (uint32_t(lane + 64 * j) < n_g) scatter_group(bo, cur.g[j], false);
-      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
-        scatter_group(bo, a.packed[cur.g0 + gi], false);
+        if (uint32_t(lane + 64 * j) < n_g) scatter_group(smem, img_base2, trash, cur.g[j], addr[j]);
+      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
+        uint32_t ad[4];
+        scatter_group(smem, img_base2, trash, a.packed[cur.g0 + gi], ad);
+      }
       __builtin_amdgcn_wave_barrier();
     }
 
@@ -369,9 +479,14 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
       __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        if (uint32_t(lane + 64 * j) < n_g) scatter_group(bo, cur.g[j], true);
-      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
-        scatter_group(bo, a.packed[cur.g0 + gi], true);
+        if (uint32_t(lane + 64 * j) < n_g) clear_group(smem, addr[j]);
+      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
+        uint32_t o01, o23;
+        const uint4 raw = a.packed[cur.g0 + gi];
+        image_offsets(raw.x, raw.y, img_base2, o01, o23);
+        const uint32_t ad[4] = {o01 & 0xFFFFu, o01 >> 16, o23 & 0xFFFFu, o23 >> 16};
+        clear_group(smem, ad);   // zeros everywhere the group could have written
+      }
     }
     if (SPARSE && MODE == 0) {
       // lane l takes groups l, l + 64, ...: the first two from the prefetch
@@ -385,28 +500,57 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
     __builtin_amdgcn_wave_barrier();
   };
 
-  // Two register buffers, both in flight: while tile t is computed from one,
-  // the loads of tile t+1 fill the other; when t is done its buffer is
-  // refilled with tile t+2.  Every issue is unconditional (past the wave's
-  // last tile it re-reads that tile, which is still in cache), so the loop is
-  // straight-line and each wait is exact: waiting for tile t leaves the NL
-  // loads of the following tile in flight.
+  // D register buffers, all in flight: while tile t is computed from one,
+  // the loads of tiles t+1 .. t+D-1 fill the others; when t is done its
+  // buffer is refilled with tile t+D.  Every issue is unconditional (past the
+  // wave's last tile it re-reads that tile, which is still in cache), so each
+  // wait is exact: waiting for tile t leaves the (D-1) NL loads of the
+  // following tiles in flight.  The loop body handles D tiles and has a
+  // single back edge, so the compiler's own load tracking sees the same order
+  // on every entry; sched_barrier keeps the scheduler from sinking a tile's
+  // loads below the next wait, which would cut the prefetch depth.
   constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
-  TileRegs<MB, MODE> ra, rb;
+  constexpr int D = pipeline_depth<MB>();
+  TileRegs<MB, MODE> rg[D];
   if (w_lo < w_hi) {
     const int last = w_hi - 1;
-    issue(w_lo, ra);
-    issue(min(w_lo + 1, last), rb);
-    for (int t = w_lo;;) {
-      wait_vmcnt<NL>();
-      compute(ra);
-      issue(min(t + 2, last), ra);
-      if (++t >= w_hi) break;
-      wait_vmcnt<NL>();
-      compute(rb);
-      issue(min(t + 2, last), rb);
-      if (++t >= w_hi) break;
+    // The first tiles' dense loads go out before the group offsets have
+    // arrived; only the group loads wait for them.
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+      load_tile_dense<MB, MODE, DENSE>(a, op, min(w_lo + i, last), n0, rg[i]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+      issue_sparse(min(w_lo + i, last), rg[i]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    auto round = [&](int t) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < D; ++i) {
+        wait_vmcnt<(D - 1) * NL>();
+        compute(rg[i]);
+        issue(min(t + i + D, last), rg[i]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    // The first round is peeled and the loop nested in it: the prologue's
+    // load order (all dense loads, then all group loads) differs from the
+    // steady state's, and the loop header must only be reached in the latter.
+    int t = w_lo;
+    if (t + D - 1 < w_hi) {
+      round(t);
+      for (t += D; t + D - 1 < w_hi; t += D) round(t);
+    }
+    // fewer than D tiles left, all already loaded: no further issue
+    static_for<0, D - 1>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      if (t + i < w_hi) {
+        wait_vmcnt<(D - 2 - i) * NL>();
+        compute(rg[i]);
+      }
+    });
   }
   __syncthreads();
 
@@ -424,6 +568,12 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
   __syncthreads();
 
   const bool split_k = a.S > 1;
+  // Partial sums cross workgroups through device-coherent (sc1) 16-byte
+  // accesses, the encoding of relaxed agent-scope atomics; no cache-wide
+  // writeback or invalidate is issued.
+  const __amdgpu_buffer_rsrc_t prs =
+      make_rsrc(a.partials, uint32_t(a.N) * uint32_t(a.S) * uint32_t(a.M) * 4u);
+  const uint32_t strip_part = uint32_t(strip) * uint32_t(a.S) * uint32_t(a.M) * 256u;  // bytes
   for (int i = tid; i < a.M * 16; i += 256) {
     const int m = i >> 4;
     const int cq = i & 15;
@@ -437,12 +587,8 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
         v += *reinterpret_cast<const f32x4_t*>(shc_all + (w * a.M + m) * 64 + 4 * cq);
     }
     if (split_k) {
-      // Partial sums travel through device-coherent (agent-scope) stores and
-      // loads, so no cache-wide writeback or invalidate is needed.
-      float* dst = a.partials + ((size_t(strip) * a.S + split) * a.M + m) * 64 + 4 * cq;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        __hip_atomic_store(dst + j, v[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t off = strip_part + uint32_t(split * a.M + m) * 256u + uint32_t(cq) * 16u;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), prs, int(off), 0, kSc1);
     } else {
       store_out(a, m, n0 + 4 * cq, v);
     }
@@ -457,15 +603,25 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
     }
     __syncthreads();
     if (*flag) {
+      // The last workgroup of the strip adds the partials in split order,
+      // with up to eight loads in flight per thread.
+      constexpr int kBatch = 8;
       for (int i = tid; i < a.M * 16; i += 256) {
         const int m = i >> 4;
         const int cq = i & 15;
+        const uint32_t base = strip_part + uint32_t(m) * 256u + uint32_t(cq) * 16u;
+        const uint32_t split_stride = uint32_t(a.M) * 256u;
         f32x4_t v{0.f, 0.f, 0.f, 0.f};
-        for (int sp = 0; sp < a.S; ++sp) {
-          const float* src = a.partials + ((size_t(strip) * a.S + sp) * a.M + m) * 64 + 4 * cq;
+        for (int s0 = 0; s0 < a.S; s0 += kBatch) {
+          u32x4_t part[kBatch];
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            v[j] += __hip_atomic_load(src + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          for (int j = 0; j < kBatch; ++j) {
+            const int sp = min(s0 + j, a.S - 1);   // in range; surplus loads unused
+            part[j] = __builtin_amdgcn_raw_buffer_load_b128(prs, int(base + uint32_t(sp) * split_stride), 0, kSc1);
+          }
+#pragma unroll
+          for (int j = 0; j < kBatch; ++j)
+            if (s0 + j < a.S) v += __builtin_bit_cast(f32x4_t, part[j]);
         }
         store_out(a, m, n0 + 4 * cq, v);
       }
@@ -565,16 +721,20 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   if (p.MODE == 0) {
     p.slot_bytes = align_up(size_t(M) * kXStride * 2, 16);
   } else {
-    p.slot_bytes = sparse ? size_t(16) * 64 * 16 : 0;   // 16 B-operand blocks of 64 x 16 B
+    p.slot_bytes = sparse ? kImageBytes : 0;   // 16 B-operand blocks of 64 x 16 B
   }
   const size_t red_bytes = size_t(4) * M * kTileN * 4;
   p.off_shc = align_up(std::max(4 * p.slot_bytes, red_bytes), 16);
   const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(4) * M * kTileN * 4 : 0;
   p.off_flag = align_up(p.off_shc + shc_bytes, 16);
-  p.lds_bytes = p.off_flag + 16;
+  p.off_trash = p.off_flag + 16;
+  p.lds_bytes = p.off_trash + 16;
   if (p.lds_bytes > 160 * 1024) return false;
 
   p.partial_bytes = p.S > 1 ? size_t(p.n_strips) * p.S * M * kTileN * 4 : 0;
+  // every array is addressed with 32-bit byte offsets
+  const size_t lim = size_t(1) << 31;
+  if (size_t(K) * N / 2 >= lim || size_t(M) * K * 2 >= lim || p.partial_bytes >= lim) return false;
   p.ws_bytes = kCounterRegion + align_up(p.partial_bytes, 256);
   *pl = p;
   return true;
@@ -602,6 +762,7 @@ int launch_matmul(const Plan& pl, const MatmulPtrs& p, bool dense, bool sparse, 
   a.slot_bytes = int(pl.slot_bytes);
   a.off_shc = int(pl.off_shc);
   a.off_flag = int(pl.off_flag);
+  a.off_trash = int(pl.off_trash);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (sparse && p.n_groups == 0) {
     // No outliers: the fused launch drops its sparse half; a sparse-only

@@ -270,6 +270,9 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
     (dict(split_k=-1), "FQ_ERR_SHAPE"),
     (dict(flags=3), "FQ_ERR_UNSUPPORTED"),
     (dict(flags=1, M=5), "FQ_ERR_UNSUPPORTED"),
+    # 32-bit byte offsets: packed weights of 2^31 bytes, partial sums of 2^31 bytes
+    (dict(K=131072, N=32768), "FQ_ERR_UNSUPPORTED"),
+    (dict(M=32, K=32768, N=65536, split_k=256), "FQ_ERR_UNSUPPORTED"),
 ])
 def test_matmul_rejects_bad_problem(lib, kw, status):
     assert _call(lib, _problem(**kw)) == status
@@ -295,6 +298,7 @@ def test_matmul_rejects_bad_tilecoo(lib):
     assert _call(lib, pr, tc=_tc(packed=None)) == "FQ_ERR_NULL"
     assert _call(lib, pr, tc=_tc(packed=FAKE + 8)) == "FQ_ERR_ALIGN"
     assert _call(lib, pr, tc=_tc(n_groups=-1)) == "FQ_ERR_FORMAT"
+    assert _call(lib, pr, tc=_tc(n_groups=1 << 27)) == "FQ_ERR_UNSUPPORTED"
 
 
 def test_matmul_rejects_small_workspace(lib):
