@@ -18,9 +18,12 @@ LIB_PATH = os.path.join(HERE, LIB_NAME)
 HOST_SOURCES = ["capi.cpp", "tilecoo.cpp"]
 HIP_SOURCES = ["kernels.hip"]
 
-# Packed-fp32 VALU forms are kept out of every HIP object.
+# Packed-fp32 VALU forms are kept out of every HIP object.  MFMA results stay
+# in ordinary VGPRs (the accumulation registers would need a copy-out per
+# tile before the fp32 scale and zero-point step).
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-mllvm", "-amdgpu-mfma-vgpr-form=1",
              "-Wall", "-Wno-unused-result"]
 HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra"]
 

@@ -15,16 +15,18 @@ typedef uint32_t u32x4_t __attribute__((__vector_size__(4 * sizeof(uint32_t))));
 // INT4 -> bf16 MFMA operand.
 //
 // A 32-bit word of Wq holds the codes of 8 consecutive k of one column, code
-// j in bits 4j..4j+3.  The bf16 value 16 + q has bit pattern 0x4180 | (q << 3)
-// (exponent 2^4, q in the top four mantissa bits), so a shift and an and-or
-// turn two codes into a packed bf16 pair without any conversion instruction.
-// The pairs come out as (k0,k4), (k1,k5), (k2,k6), (k3,k7); the activation
-// operand is staged in LDS in that same order, so the 8-term dot product the
-// MFMA forms per lane is unchanged.  The offset 16 + z is removed after each
-// 128-row group with the exact identity
-//     sum_k x_k (q_k - z) = sum_k x_k (16 + q_k) - (16 + z) sum_k x_k,
+// j in bits 4j..4j+3.  The bf16 value 128 + q has bit pattern 0x4300 | q
+// (exponent 2^7, q in the low four mantissa bits, whose unit is 1), so one
+// and-or turns the codes sitting in bits 0..3 and 16..19 of a word into a
+// packed bf16 pair without any conversion instruction: the pairs come out as
+// (k0,k4), (k1,k5), (k2,k6), (k3,k7) after shifts by 0, 4, 8 and 12.  The
+// activation operand is staged in that same order, so the 8-term dot product
+// the MFMA forms per lane is unchanged.  The offset 128 + z is removed after
+// each 128-row group with the exact identity
+//     sum_k x_k (q_k - z) = sum_k x_k (128 + q_k) - (128 + z) sum_k x_k,
 // so (q - z) never needs to be formed and the scale s is applied in fp32 once
-// per group (eq. 3 of the paper).
+// per group (eq. 3 of the paper).  The fp32 sums are at most 143 sum|x_k|,
+// which keeps their rounding error near 1e-6 of the result.
 // ---------------------------------------------------------------------------
 // (a & b) | c as one VALU operation (gfx950 three-input bitwise op; truth
 // table 0xEA).  Plain C++ for this pattern compiles to two VOP2 operations,
@@ -33,13 +35,15 @@ __device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
   return __builtin_amdgcn_bitop3_b32(a, b, c, 0xEA);
 }
 
+constexpr float kCodeOffset = 128.f;   // value of the bf16 bit pattern 0x4300
+
 __device__ __forceinline__ bf16x8_t dequant_word(uint32_t w) {
-  const uint32_t mask = 0x00780078u, bias = 0x41804180u;
+  const uint32_t mask = 0x000F000Fu, bias = 0x43004300u;
   u32x4_t r;
-  r[0] = and_or(w << 3, mask, bias);
-  r[1] = and_or(w >> 1, mask, bias);
-  r[2] = and_or(w >> 5, mask, bias);
-  r[3] = and_or(w >> 9, mask, bias);
+  r[0] = and_or(w, mask, bias);
+  r[1] = and_or(w >> 4, mask, bias);
+  r[2] = and_or(w >> 8, mask, bias);
+  r[3] = and_or(w >> 12, mask, bias);
   return __builtin_bit_cast(bf16x8_t, r);
 }
 
@@ -51,7 +55,7 @@ __device__ __forceinline__ uint32_t chunk_pos(uint32_t k) {
 
 // Same map applied to four packed u8 row indices at once.
 __device__ __forceinline__ uint32_t chunk_pos4(uint32_t k4) {
-  return (k4 & 0xF8F8F8F8u) | ((k4 & 0x03030303u) << 1) | ((k4 >> 2) & 0x01010101u);
+  return and_or(k4, 0xF8F8F8F8u, and_or(k4 << 1, 0x06060606u, (k4 >> 2) & 0x01010101u));
 }
 
 // 16 bytes of X (x0..x7) -> chunk order (x0,x4,x1,x5,x2,x6,x3,x7): one byte

@@ -15,11 +15,11 @@
 //             contiguously, so one load of tile_indptr gives every range).
 //             While tile t is computed, tile t+1 is in flight (Sec. 4.1).
 //   dense     per 32-row step a lane turns 8 codes of each of its 4 columns
-//             into bf16 (16 + q) operands in registers and issues
+//             into bf16 (128 + q) operands in registers and issues
 //             v_mfma_f32_16x16x32_bf16 against X; one more MFMA against an
 //             all-ones operand yields the per-row sums of X.  After the group:
-//             acc += s * (sum x (16+q) - (16+z) sum x), i.e. eq. (3) applied
-//             exactly once per (group, column) in fp32.
+//             acc += s * (sum x (128+q) - (128+z) sum x), i.e. eq. (3) applied
+//             once per (group, column) in fp32.
 //   sparse    (Sec. 3.1 thread level, Sec. 4.2 decoding) two mappings of the
 //             same Tile-COO groups, chosen by the number of rows M:
 //     M <= 4  the tile's X slice sits in the wave's LDS slot; each lane decodes
@@ -51,6 +51,7 @@
 namespace fqk {
 
 constexpr int XS = fqi::kXStride;   // LDS row stride of a staged X slice, elements
+constexpr int kGatherLimitM = fqi::kGatherLimitM;
 
 struct MatmulArgs {
   const uint16_t* X;
@@ -216,22 +217,19 @@ __device__ __forceinline__ void sparse_gather(const MatmulArgs& a, const uint16_
   const uint32_t p2 = (p4 >> 16) & 0xFFu, p3 = p4 >> 24;
   if (single_column(d)) {
     float* out = shc + (d.cols & 63u);
-    for (int m0 = 0; m0 < a.M; m0 += 4) {
-      // four rows at a time: all sixteen gathers issued before any use
-      uint32_t x01[4], x23[4];
+    // only the M <= 4 real rows: every gather of a row is issued before any use
+    uint32_t x01[kGatherLimitM], x23[kGatherLimitM];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint16_t* xr = xs + min(m0 + j, a.M - 1) * XS;
-        x01[j] = uint32_t(xr[p0]) | (uint32_t(xr[p1]) << 16);
-        x23[j] = uint32_t(xr[p2]) | (uint32_t(xr[p3]) << 16);
+    for (int m = 0; m < kGatherLimitM; ++m) {
+      if (m < a.M) {
+        const uint16_t* xr = xs + m * XS;
+        x01[m] = __builtin_amdgcn_perm(uint32_t(xr[p1]), uint32_t(xr[p0]), 0x05040100u);
+        x23[m] = __builtin_amdgcn_perm(uint32_t(xr[p3]), uint32_t(xr[p2]), 0x05040100u);
       }
-      float part[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) part[j] = dot2_bf16(x23[j], d.v23, dot2_bf16(x01[j], d.v01, 0.f));
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (m0 + j < a.M) atomicAdd(out + (m0 + j) * 64, part[j]);
     }
+#pragma unroll
+    for (int m = 0; m < kGatherLimitM; ++m)
+      if (m < a.M) atomicAdd(out + m * 64, dot2_bf16(x23[m], d.v23, dot2_bf16(x01[m], d.v01, 0.f)));
   } else {
     const uint32_t pj[4] = {p0, p1, p2, p3};
     for (int m = 0; m < a.M; ++m) {
@@ -454,7 +452,7 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
       sc[3] = f16_bits_to_f32(cur.s.y >> 16);
       const int zsh = (c4 & 1) * 16;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) zf[c] = 16.f + float((cur.z >> (zsh + 4 * c)) & 15u);
+      for (int c = 0; c < 4; ++c) zf[c] = kCodeOffset + float((cur.z >> (zsh + 4 * c)) & 15u);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
