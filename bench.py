@@ -37,7 +37,7 @@ SHAPES = [("qkv", 4096, 6144), ("o", 4096, 4096), ("gate_up", 4096, 28672),
           ("down", 14336, 4096)]
 MS = [1, 4, 8, 16]
 FRAC = 0.01
-DOMINANT_MIN_M = 4          # the fused kernel's MFMA sparse mapping serves M >= 4
+DOMINANT_MIN_M = 4          # the step's M >= 4 matmuls: fused kernel, MFMA sparse mapping
 COPY_CAL_BYTES = 256 << 20  # plain device copy used to calibrate FETCH_SIZE / WRITE_SIZE
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fused_llama3_8b_decode_traffic.md")
 
@@ -306,9 +306,9 @@ def main():
             del Ws
             torch.cuda.empty_cache()
 
-    # Dominant kernel: the fused kernel with the MFMA sparse mapping (M >= 4),
-    # which takes most of the step; the gather mapping (M <= 3) is reported
-    # beside it.
+    # Dominant kernel: the fused kernel with the MFMA sparse mapping (the step's
+    # M = 4, 8, 16 matmuls), which takes most of the step; the M = 1 matmuls
+    # (gather mapping) are reported beside it.
     def agg(sel):
         b = sum(d["bytes"] for d in details if sel(d))
         t = sum(d["fused_us"] for d in details if sel(d))
@@ -342,7 +342,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "matmul_kernel<1, 1, true, true> (fused, MFMA sparse mapping, M=4,8,16)",
+            "kernel": "matmul_kernel<1, 1, true, true, NW> (fused, MFMA sparse mapping, M=4,8,16)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",

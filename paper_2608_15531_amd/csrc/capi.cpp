@@ -102,12 +102,21 @@ fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes) {
   if (!bytes) return FQ_ERR_NULL;
   fq_status st = check_problem(pr);
   if (st != FQ_OK) return st;
-  fqi::Plan a, b;
-  // Dense and sparse plans share the split choice; take the larger layout.
-  if (!fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, true, true, 1, 0, &a) ||
-      !fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, true, false, 0, 0, &b))
-    return FQ_ERR_UNSUPPORTED;
-  *bytes = a.ws_bytes > b.ws_bytes ? a.ws_bytes : b.ws_bytes;
+  // The split, and with it the partial-sum area, depends on the kernel the
+  // call launches: size for the largest of dense-only and both mappings.
+  fqi::Plan pl;
+  size_t need = 0;
+  bool any = false;
+  for (int mode = -1; mode <= 1; ++mode) {
+    for (int sparse = 0; sparse <= 1; ++sparse) {
+      if (fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, true, sparse != 0, 1, 0, &pl, mode)) {
+        any = true;
+        need = pl.ws_bytes > need ? pl.ws_bytes : need;
+      }
+    }
+  }
+  if (!any) return FQ_ERR_UNSUPPORTED;
+  *bytes = need;
   return FQ_OK;
 }
 

@@ -9,11 +9,10 @@ namespace fqi {
 
 constexpr int kTileK = 128;     // K side of a dense/sparse tile = quantisation group
 constexpr int kTileN = 64;      // N side of a tile = one output strip
-constexpr int kThreads = 256;   // four wave64 per workgroup
 constexpr int kMaxM = 32;       // rows the fused GEMV-regime kernel supports
 constexpr int kMaxBuckets = 256;
 constexpr int kXStride = 136;   // LDS row stride (elements) of a staged 128-wide X slice
-constexpr int kGatherMaxM = 3;  // up to this M the sparse path gathers X in LDS; above, MFMA
+constexpr int kGatherMaxM = 1;  // up to this M the sparse path gathers X in LDS; above, MFMA
 constexpr int kGatherLimitM = 4; // rows the gather mapping can stage at all
 constexpr int kImageBytes = 16384;   // one wave's B-operand image of a 128 x 64 tile
 // The workspace starts with a fixed counter region (one uint32 per 64-column
@@ -32,6 +31,7 @@ struct Plan {
   int n_strips;      // N / 64
   int T;             // tiles per strip, K / 128
   int S;             // K ranges per strip (split-K)
+  int NW;            // waves per workgroup: 4 or 8
   int B;             // buckets per tile
   // dynamic LDS layout, bytes: four wave slots (X slice or B-operand image),
   // then the gather-mode sparse output buffers

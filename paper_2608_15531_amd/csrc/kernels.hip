@@ -22,16 +22,19 @@
 //             once per (group, column) in fp32.
 //   sparse    (Sec. 3.1 thread level, Sec. 4.2 decoding) two mappings of the
 //             same Tile-COO groups, chosen by the number of rows M:
-//     M <= 4  the tile's X slice sits in the wave's LDS slot; each lane decodes
+//     M = 1   the tile's X slice sits in the wave's LDS slot; each lane decodes
 //             one group, gathers X[m][k] for every row and accumulates v * x
-//             with v_dot2_f32_bf16 into the wave's LDS output buffer.
-//     M >= 5  each lane scatters its group's values into an LDS buffer laid out
-//             as the MFMA B operand of the tile (zero elsewhere); the wave reads
-//             it back with conflict-free 128-bit reads and issues 16 MFMAs
-//             against the same X fragments straight into the register output
-//             tile, then restores the zeros.  bf16 x bf16 products are exact in
-//             the fp32 accumulator, so this is the SpMM of eq. (1) on the
-//             matrix cores, with its cost independent of M.
+//             with v_dot2_f32_bf16 into the wave's LDS output buffer (the
+//             mapping also serves M <= 4 on request).
+//     M >= 2  each lane scatters its group's values into an LDS buffer laid out
+//             as the MFMA B operand of the tile (zero elsewhere); per 32-row
+//             step the wave reads the step's four blocks back with
+//             conflict-free 128-bit reads and issues four MFMAs against the
+//             same X fragments straight into the register output tile; the
+//             zeros are restored after the tile.  bf16 x bf16 products are
+//             exact in the fp32 accumulator, so this is the SpMM of eq. (1) on
+//             the matrix cores, with its cost independent of M.  When the
+//             strips fit the CUs this kernel runs eight waves per workgroup.
 //   reduce    after the loop the four waves' register tiles (and sparse
 //             buffers) are summed in LDS in a fixed order.  With split-K each
 //             workgroup stores its fp32 partial with device-coherent stores
@@ -208,39 +211,58 @@ __device__ __forceinline__ void store_out(const MatmulArgs& a, int m, int n, f32
   }
 }
 
-// Gather mode: one group held by this lane, all rows, into the wave's buffer.
+// Gather mode, single-column groups (every group in by-column mode): the X
+// values of the group's four rows for each of the M <= 4 rows, read from the
+// staged slice.  Issued before the dense work of the tile and consumed after
+// it, so the LDS latency hides behind the dequantisation.
+struct Gathered {
+  uint32_t x01[kGatherLimitM], x23[kGatherLimitM];   // x[k0] | x[k1] << 16, x[k2] | x[k3] << 16
+};
+
+__device__ __forceinline__ void gather_x(const MatmulArgs& a, const uint16_t* xs, uint4 raw,
+                                         Gathered& g) {
+  const uint32_t p4 = chunk_pos4(raw.x & 0x7F7F7F7Fu);
+  const uint32_t p0 = p4 & 0xFFu, p1 = (p4 >> 8) & 0xFFu;
+  const uint32_t p2 = (p4 >> 16) & 0xFFu, p3 = p4 >> 24;
+#pragma unroll
+  for (int m = 0; m < kGatherLimitM; ++m) {
+    if (m < a.M) {
+      const uint16_t* xr = xs + m * XS;
+      g.x01[m] = __builtin_amdgcn_perm(uint32_t(xr[p1]), uint32_t(xr[p0]), 0x05040100u);
+      g.x23[m] = __builtin_amdgcn_perm(uint32_t(xr[p3]), uint32_t(xr[p2]), 0x05040100u);
+    }
+  }
+}
+
+// sum_j v_j x[m][k_j] for each row, added to the wave's buffer at the column.
+__device__ __forceinline__ void gather_add(const MatmulArgs& a, uint4 raw, const Gathered& g,
+                                           float* shc) {
+  float* out = shc + (raw.y & 63u);
+#pragma unroll
+  for (int m = 0; m < kGatherLimitM; ++m)
+    if (m < a.M) atomicAdd(out + m * 64, dot2_bf16(g.x23[m], raw.w, dot2_bf16(g.x01[m], raw.z, 0.f)));
+}
+
+// Gather mode, any group (slots may sit in different columns): one product
+// per real slot and row.
 __device__ __forceinline__ void sparse_gather(const MatmulArgs& a, const uint16_t* xs, uint4 raw,
                                               float* shc) {
   const Group d = decode_group(raw);
-  const uint32_t p4 = chunk_pos4(d.rows & 0x7F7F7F7Fu);
-  const uint32_t p0 = p4 & 0xFFu, p1 = (p4 >> 8) & 0xFFu;
-  const uint32_t p2 = (p4 >> 16) & 0xFFu, p3 = p4 >> 24;
   if (single_column(d)) {
-    float* out = shc + (d.cols & 63u);
-    // only the M <= 4 real rows: every gather of a row is issued before any use
-    uint32_t x01[kGatherLimitM], x23[kGatherLimitM];
+    Gathered g;
+    gather_x(a, xs, raw, g);
+    gather_add(a, raw, g, shc);
+    return;
+  }
+  const uint32_t p4 = chunk_pos4(d.rows & 0x7F7F7F7Fu);
+  for (int m = 0; m < a.M; ++m) {
+    const uint16_t* xr = xs + m * XS;
 #pragma unroll
-    for (int m = 0; m < kGatherLimitM; ++m) {
-      if (m < a.M) {
-        const uint16_t* xr = xs + m * XS;
-        x01[m] = __builtin_amdgcn_perm(uint32_t(xr[p1]), uint32_t(xr[p0]), 0x05040100u);
-        x23[m] = __builtin_amdgcn_perm(uint32_t(xr[p3]), uint32_t(xr[p2]), 0x05040100u);
-      }
-    }
-#pragma unroll
-    for (int m = 0; m < kGatherLimitM; ++m)
-      if (m < a.M) atomicAdd(out + m * 64, dot2_bf16(x23[m], d.v23, dot2_bf16(x01[m], d.v01, 0.f)));
-  } else {
-    const uint32_t pj[4] = {p0, p1, p2, p3};
-    for (int m = 0; m < a.M; ++m) {
-      const uint16_t* xr = xs + m * XS;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t v = slot_val(d, j);
-        if (v != 0u)
-          atomicAdd(shc + m * 64 + (slot_col(d, j) & 63u),
-                    bf16_bits_to_f32(xr[pj[j]]) * bf16_bits_to_f32(v));
-      }
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t v = slot_val(d, j);
+      if (v != 0u)
+        atomicAdd(shc + m * 64 + (slot_col(d, j) & 63u),
+                  bf16_bits_to_f32(xr[(p4 >> (8 * j)) & 0xFFu]) * bf16_bits_to_f32(v));
     }
   }
 }
@@ -252,10 +274,8 @@ __device__ __forceinline__ void sparse_gather(const MatmulArgs& a, const uint16_
 //   0: k2 | 1-2: k0,k1 | 3-6: n2..n5 | 7-8: k3,k4 | 9-10: n0,n1 | 11-12: k5,k6.
 // image_offsets forms the four byte offsets of a group at once, one slot per
 // byte lane while the index is split into its low and high bytes, then two
-// slots per dword (16-bit halves), with the slot's base folded in (the four
-// wave images fill the first 64 KB of LDS, so every offset fits 16 bits).
-__device__ __forceinline__ void image_offsets(uint32_t R, uint32_t C, uint32_t base2,
-                                              uint32_t& o01, uint32_t& o23) {
+// slots per dword (16-bit halves; the offsets are below 2^14).
+__device__ __forceinline__ void image_offsets(uint32_t R, uint32_t C, uint32_t& o01, uint32_t& o23) {
   const uint32_t r1 = R << 1, r2 = R >> 2, c1 = C << 1;
   uint32_t lo = r2 & 0x01010101u;               // k2
   lo = and_or(r1, 0x06060606u, lo);             // k0, k1
@@ -264,36 +284,49 @@ __device__ __forceinline__ void image_offsets(uint32_t R, uint32_t C, uint32_t b
   uint32_t hi = (R >> 4) & 0x01010101u;         // k4
   hi = and_or(c1, 0x06060606u, hi);             // n0, n1
   hi = and_or(r2, 0x18181818u, hi);             // k5, k6
-  // [lo0 hi0 lo1 hi1] and [lo2 hi2 lo3 hi3]: indices < 2^13, so doubling and
-  // adding the base never carries across the halves
-  o01 = (__builtin_amdgcn_perm(hi, lo, 0x05010400u) << 1) + base2;
-  o23 = (__builtin_amdgcn_perm(hi, lo, 0x07030602u) << 1) + base2;
+  // [lo0 hi0 lo1 hi1] and [lo2 hi2 lo3 hi3], then element -> byte offset
+  o01 = __builtin_amdgcn_perm(hi, lo, 0x05010400u) << 1;
+  o23 = __builtin_amdgcn_perm(hi, lo, 0x07030602u) << 1;
 }
 
-// Writes a group's four values into the image and returns where they went:
-// a padding slot (value bits 0) goes to the trash word instead, since its
-// position may coincide with a real element of another group.
-__device__ __forceinline__ void scatter_group(unsigned char* smem, uint32_t base2, uint32_t trash,
-                                              uint4 raw, uint32_t addr[4]) {
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+
+// 16-bit LDS store at an absolute LDS byte address.
+__device__ __forceinline__ void lds_store16(uint32_t addr, uint32_t v) {
+  *reinterpret_cast<lds_u16*>(uintptr_t(addr)) = uint16_t(v);
+}
+
+// LDS byte address where a dynamic-LDS pointer points.
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return uint32_t(reinterpret_cast<uintptr_t>(
+      (__attribute__((address_space(3))) const unsigned char*)(p)));
+}
+
+// Writes a group's four values into the image at absolute LDS address `img`
+// and returns where they went: a padding slot (value bits 0) goes to the
+// trash word instead, since its position may coincide with a real element of
+// another group.
+__device__ __forceinline__ void scatter_group(uint32_t img, uint32_t trash, uint4 raw,
+                                              uint32_t addr[4]) {
   uint32_t o01, o23;
-  image_offsets(raw.x, raw.y, base2, o01, o23);
-  addr[0] = (raw.z & 0xFFFFu) != 0u ? (o01 & 0xFFFFu) : trash;
-  addr[1] = raw.z > 0xFFFFu ? (o01 >> 16) : trash;
-  addr[2] = (raw.w & 0xFFFFu) != 0u ? (o23 & 0xFFFFu) : trash;
-  addr[3] = raw.w > 0xFFFFu ? (o23 >> 16) : trash;
-  *reinterpret_cast<uint16_t*>(smem + addr[0]) = uint16_t(raw.z);
-  *reinterpret_cast<uint16_t*>(smem + addr[1]) = uint16_t(raw.z >> 16);
-  *reinterpret_cast<uint16_t*>(smem + addr[2]) = uint16_t(raw.w);
-  *reinterpret_cast<uint16_t*>(smem + addr[3]) = uint16_t(raw.w >> 16);
+  image_offsets(raw.x, raw.y, o01, o23);
+  addr[0] = (raw.z & 0xFFFFu) != 0u ? img + (o01 & 0xFFFFu) : trash;
+  addr[1] = raw.z > 0xFFFFu ? img + (o01 >> 16) : trash;
+  addr[2] = (raw.w & 0xFFFFu) != 0u ? img + (o23 & 0xFFFFu) : trash;
+  addr[3] = raw.w > 0xFFFFu ? img + (o23 >> 16) : trash;
+  lds_store16(addr[0], raw.z);
+  lds_store16(addr[1], raw.z >> 16);
+  lds_store16(addr[2], raw.w);
+  lds_store16(addr[3], raw.w >> 16);
 }
 
-__device__ __forceinline__ void clear_group(unsigned char* smem, const uint32_t addr[4]) {
+__device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) *reinterpret_cast<uint16_t*>(smem + addr[j]) = 0;
+  for (int j = 0; j < 4; ++j) lds_store16(addr[j], 0u);
 }
 
-template <int MB, int MODE, bool DENSE, bool SPARSE>
-__global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
+template <int MB, int MODE, bool DENSE, bool SPARSE, int NW>
+__global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -313,8 +346,8 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
   const int t_lo = int(int64_t(split) * a.T / a.S);
   const int t_hi = int(int64_t(split + 1) * a.T / a.S);
   const int nt = t_hi - t_lo;
-  const int w_lo = t_lo + (nt * wave) / 4;     // this wave's tiles [w_lo, w_hi)
-  const int w_hi = t_lo + (nt * (wave + 1)) / 4;
+  const int w_lo = t_lo + (nt * wave) / NW;    // this wave's tiles [w_lo, w_hi)
+  const int w_hi = t_lo + (nt * (wave + 1)) / NW;
   const int n0 = strip * 64;
   const int64_t tile_base = int64_t(strip) * a.T;
 
@@ -368,9 +401,8 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
     for (int mb = 0; mb < MB; ++mb)   // rows past M load row M-1, never stored
       op.lx[mb] = (uint32_t(min(mb * 16 + c4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(h)) * 2u;
   }
-  const uint32_t img_base = uint32_t(wave) * uint32_t(a.slot_bytes);
-  const uint32_t img_base2 = img_base | (img_base << 16);
-  const uint32_t trash = uint32_t(a.off_trash);
+  const uint32_t img = lds_address(bo);                  // this wave's image
+  const uint32_t trash = lds_address(smem + a.off_trash);
 
   auto issue_sparse = [&](int t, TileRegs<MB, MODE>& r) __attribute__((always_inline)) {
     uint32_t g0 = 0, g1 = 0;
@@ -414,25 +446,46 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
     if (SPARSE && MODE == 1) {
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        if (uint32_t(lane + 64 * j) < n_g) scatter_group(smem, img_base2, trash, cur.g[j], addr[j]);
+        if (uint32_t(lane + 64 * j) < n_g) scatter_group(img, trash, cur.g[j], addr[j]);
       for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
         uint32_t ad[4];
-        scatter_group(smem, img_base2, trash, a.packed[cur.g0 + gi], ad);
+        scatter_group(img, trash, a.packed[cur.g0 + gi], ad);
       }
       __builtin_amdgcn_wave_barrier();
     }
 
-    // ---- dense path
-    if (DENSE) {
-      f32x4_t tmp[MB][4], xsum[MB];
+    // ---- gather mapping: the first two groups' X values, read before the
+    // dense work so their LDS latency is hidden
+    Gathered gx[2];
+    bool gsingle[2] = {false, false};
+    if (SPARSE && MODE == 0) {
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        xsum[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < 4; ++c) tmp[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < 2; ++j) {
+        gsingle[j] = uint32_t(lane + 64 * j) < n_g && single_column(decode_group(cur.g[j]));
+        if (gsingle[j]) gather_x(a, xs, cur.g[j], gx[j]);
       }
+    }
+
+    // ---- dense path, with the MFMA mapping's outlier MFMAs interleaved per
+    // 32-row step: the step's four image blocks are read from LDS before its
+    // dequantisation and multiplied after it
+    constexpr bool SPM = SPARSE && MODE == 1;
+    const uint4* b4 = reinterpret_cast<const uint4*>(bo);
+    f32x4_t tmp[MB][4], xsum[MB];
 #pragma unroll
-      for (int step = 0; step < 4; ++step) {
+    for (int mb = 0; mb < MB; ++mb) {
+      xsum[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) tmp[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int step = 0; step < 4; ++step) {
+      bf16x8_t Bo[4];
+      if (SPM) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) Bo[c] = __builtin_bit_cast(bf16x8_t, b4[(step * 4 + c) * 64 + lane]);
+      }
+      if (DENSE) {
         const uint32_t w4[4] = {cur.w[step].x, cur.w[step].y, cur.w[step].z, cur.w[step].w};
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
@@ -445,6 +498,15 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
         for (int mb = 0; mb < MB; ++mb)
           xsum[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], ones, xsum[mb], 0, 0, 0);
       }
+      if (SPM) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+            acc[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bo[c], acc[mb][c], 0, 0, 0);
+      }
+    }
+    if (DENSE) {
       float sc[4], zf[4];
       sc[0] = f16_bits_to_f32(cur.s.x & 0xFFFFu);
       sc[1] = f16_bits_to_f32(cur.s.x >> 16);
@@ -462,36 +524,28 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
             acc[mb][c][r] += sc[c] * (tmp[mb][c][r] - zf[c] * xsum[mb][r]);
     }
 
-    // ---- sparse path
-    if (SPARSE && MODE == 1) {
-      const uint4* b4 = reinterpret_cast<const uint4*>(bo);
-#pragma unroll
-      for (int step = 0; step < 4; ++step)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const bf16x8_t Bo = __builtin_bit_cast(bf16x8_t, b4[(step * 4 + c) * 64 + lane]);
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
-            acc[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bo, acc[mb][c], 0, 0, 0);
-        }
+    // ---- MFMA mapping: restore the zeros of the image
+    if (SPM) {
       __builtin_amdgcn_wave_barrier();
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        if (uint32_t(lane + 64 * j) < n_g) clear_group(smem, addr[j]);
+        if (uint32_t(lane + 64 * j) < n_g) clear_group(addr[j]);
       for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
         uint32_t o01, o23;
         const uint4 raw = a.packed[cur.g0 + gi];
-        image_offsets(raw.x, raw.y, img_base2, o01, o23);
-        const uint32_t ad[4] = {o01 & 0xFFFFu, o01 >> 16, o23 & 0xFFFFu, o23 >> 16};
-        clear_group(smem, ad);   // zeros everywhere the group could have written
+        image_offsets(raw.x, raw.y, o01, o23);
+        const uint32_t ad[4] = {img + (o01 & 0xFFFFu), img + (o01 >> 16), img + (o23 & 0xFFFFu),
+                                img + (o23 >> 16)};
+        clear_group(ad);   // zeros everywhere the group could have written
       }
     }
+    // ---- gather mapping: finish the first two groups, then any further ones
     if (SPARSE && MODE == 0) {
-      // lane l takes groups l, l + 64, ...: the first two from the prefetch
-      // registers, any further ones straight from memory
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        if (uint32_t(lane + 64 * j) < n_g) sparse_gather(a, xs, cur.g[j], shc);
+      for (int j = 0; j < 2; ++j) {
+        if (gsingle[j]) gather_add(a, cur.g[j], gx[j], shc);
+        else if (uint32_t(lane + 64 * j) < n_g) sparse_gather(a, xs, cur.g[j], shc);
+      }
       for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
         sparse_gather(a, xs, a.packed[cur.g0 + gi], shc);
     }
@@ -572,16 +626,16 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
   const __amdgpu_buffer_rsrc_t prs =
       make_rsrc(a.partials, uint32_t(a.N) * uint32_t(a.S) * uint32_t(a.M) * 4u);
   const uint32_t strip_part = uint32_t(strip) * uint32_t(a.S) * uint32_t(a.M) * 256u;  // bytes
-  for (int i = tid; i < a.M * 16; i += 256) {
+  for (int i = tid; i < a.M * 16; i += 64 * NW) {
     const int m = i >> 4;
     const int cq = i & 15;
     f32x4_t v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
+    for (int w = 0; w < NW; ++w)
       v += *reinterpret_cast<const f32x4_t*>(red + (w * a.M + m) * 64 + 4 * cq);
     if (SPARSE && MODE == 0) {
 #pragma unroll
-      for (int w = 0; w < 4; ++w)
+      for (int w = 0; w < NW; ++w)
         v += *reinterpret_cast<const f32x4_t*>(shc_all + (w * a.M + m) * 64 + 4 * cq);
     }
     if (split_k) {
@@ -604,7 +658,7 @@ __global__ void __launch_bounds__(256) matmul_kernel(MatmulArgs a) {
       // The last workgroup of the strip adds the partials in split order,
       // with up to eight loads in flight per thread.
       constexpr int kBatch = 8;
-      for (int i = tid; i < a.M * 16; i += 256) {
+      for (int i = tid; i < a.M * 16; i += 64 * NW) {
         const int m = i >> 4;
         const int cq = i & 15;
         const uint32_t base = strip_part + uint32_t(m) * 256u + uint32_t(cq) * 16u;
@@ -654,9 +708,9 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
   }
 }
 
-template <int MB, int MODE, bool DENSE, bool SPARSE>
+template <int MB, int MODE, bool DENSE, bool SPARSE, int NW>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, MODE, DENSE, SPARSE>;
+  auto kern = matmul_kernel<MB, MODE, DENSE, SPARSE, NW>;
   if (pl.lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -664,15 +718,21 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
     if (e != hipSuccess) return int(e);
   }
   const unsigned grid = unsigned(pl.n_strips) * unsigned(pl.S);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(256), pl.lds_bytes, stream, args);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * NW), pl.lds_bytes, stream, args);
   return int(hipGetLastError());
+}
+
+template <int MB, int MODE, int NW>
+int launch_waves(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
+  if (dense && sparse) return launch_variant<MB, MODE, true, true, NW>(pl, a, s);
+  if (dense) return launch_variant<MB, MODE, true, false, NW>(pl, a, s);
+  return launch_variant<MB, MODE, false, true, NW>(pl, a, s);
 }
 
 template <int MB, int MODE>
 int launch_mode(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
-  if (dense && sparse) return launch_variant<MB, MODE, true, true>(pl, a, s);
-  if (dense) return launch_variant<MB, MODE, true, false>(pl, a, s);
-  return launch_variant<MB, MODE, false, true>(pl, a, s);
+  return pl.NW == 8 ? launch_waves<MB, MODE, 8>(pl, a, dense, sparse, s)
+                    : launch_waves<MB, MODE, 4>(pl, a, dense, sparse, s);
 }
 
 }  // namespace fqk
@@ -682,15 +742,27 @@ namespace fqi {
 namespace {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-int default_split(int T, int n_strips) {
-  // At least about 256 workgroups (one per CU, four waves each), at least one
-  // tile per wave; wide matrices need no split at all.  Measured on the
-  // Llama-3 decode shapes: 4096 x {4096, 6144} and 14336 x 4096 run best at
-  // 4 splits, 4096 x 28672 unsplit.
+// Grid shape.  The fused kernel with the MFMA outlier mapping is bound by
+// per-SIMD issue (dequantisation VALU, MFMA and the LDS image of the
+// outliers), so when the strips fit the CUs it runs eight waves per
+// workgroup -- two per SIMD, overlapping one another's VALU, MFMA and LDS
+// work -- with the largest split that keeps at most one workgroup per CU
+// and one tile per wave.  Otherwise (dense only, the gather mapping, or more
+// strips than CUs) four waves per workgroup and the smallest split that
+// reaches about one workgroup per CU, at least one tile per wave; wide
+// matrices need no split.
+int default_split(int T, int n_strips, bool eight_waves) {
   int S = 1;
-  while (S * n_strips < 256) S *= 2;
-  S = std::min(S, std::max(1, T / 4));
-  return std::max(S, 1);
+  if (eight_waves && n_strips <= 256) {
+    while (int64_t(n_strips) * 2 * S <= 256 && T / (2 * S) >= 8) S *= 2;
+    return S;
+  }
+  while (int64_t(n_strips) * S < 256 && 2 * S <= T / 4) S *= 2;
+  return S;
+}
+
+int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
+  return (eight_waves && int64_t(n_strips) * S <= 256 && T / S >= 8) ? 8 : 4;
 }
 }  // namespace
 
@@ -710,10 +782,12 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   if (p.MODE == 0 && M > kGatherLimitM) return false;
   p.n_strips = N / kTileN;
   p.T = K / kTileK;
-  int S = split_k > 0 ? split_k : default_split(p.T, p.n_strips);
+  const bool eight = sparse && p.MODE == 1;
+  int S = split_k > 0 ? split_k : default_split(p.T, p.n_strips, eight);
   // each wave indexes its tiles' group offsets from one register: <= 63 tiles
   S = std::max(S, (p.T + 4 * 63 - 1) / (4 * 63));
   p.S = std::max(1, std::min(S, p.T));
+  p.NW = waves_per_workgroup(p.T, p.S, p.n_strips, eight);
   p.B = sparse ? B : 1;
 
   if (p.MODE == 0) {
@@ -721,9 +795,9 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   } else {
     p.slot_bytes = sparse ? kImageBytes : 0;   // 16 B-operand blocks of 64 x 16 B
   }
-  const size_t red_bytes = size_t(4) * M * kTileN * 4;
-  p.off_shc = align_up(std::max(4 * p.slot_bytes, red_bytes), 16);
-  const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(4) * M * kTileN * 4 : 0;
+  const size_t red_bytes = size_t(p.NW) * M * kTileN * 4;
+  p.off_shc = align_up(std::max(p.NW * p.slot_bytes, red_bytes), 16);
+  const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * M * kTileN * 4 : 0;
   p.off_flag = align_up(p.off_shc + shc_bytes, 16);
   p.off_trash = p.off_flag + 16;
   p.lds_bytes = p.off_trash + 16;
