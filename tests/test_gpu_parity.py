@@ -9,6 +9,7 @@ Bars:
   fp32 Y Frobenius relative error <= 1e-4.
 """
 
+import dataclasses
 import os
 
 import numpy as np
@@ -244,3 +245,58 @@ def test_full_size_sampled_columns(gpu_lib, shape, M):
     yu = run(gpu_lib, prob, "unfused", "f32")
     rel = np.linalg.norm(yu - y32) / np.linalg.norm(y32)
     assert rel <= F32_FROB
+
+
+# --------------------------------------- density sweep at its real shape --
+
+@pytest.mark.parametrize("frac", [0.0, 0.005, 0.01, 0.02, 0.05])
+@pytest.mark.parametrize("dist", ["uniform", "clustered"])
+def test_density_sweep_full_shape(gpu_lib, frac, dist):
+    """M = 8, 4096 x 14336, outlier fraction 0-5 %, uniform or column-clustered
+    (2 % of the columns take half of the outliers, capped when they fill up);
+    sampled columns against the oracle, every column against the unfused path."""
+    K, N, M = 4096, 14336, 8
+    log(f"density full frac={frac} {dist}")
+    prob = make_problem(M, K, N, frac=frac, dist=dist,
+                        seed=seed_for(2, 0, 0) + int(frac * 1000) + (dist == "clustered"))
+    rng = np.random.default_rng(K + N + int(frac * 1000))
+    heavy = np.unique(prob.n)[:32] if prob.n.size else np.array([], dtype=np.int64)
+    cols = np.unique(np.concatenate([[0, N - 1], heavy, rng.choice(N, 96, replace=False)]))
+    y_ref = ref(prob, cols)
+    assert_bf16_close(run(gpu_lib, prob, "fused", "bf16")[:, cols], y_ref)
+    y32 = run(gpu_lib, prob, "fused", "f32")
+    assert_f32_close(y32[:, cols], y_ref)
+    yu = run(gpu_lib, prob, "unfused", "f32")
+    assert np.linalg.norm(yu - y32) <= F32_FROB * max(np.linalg.norm(y32), 1e-30)
+
+
+# ------------------------------------------ Llama-3-70B decode linears --
+
+SHAPES_70B = [(8192, 10240), (8192, 8192), (8192, 57344), (28672, 8192)]
+_PROBLEMS_70B = {}
+
+
+def _problem_70b(shape, M):
+    """One weight set per shape (drawn at M = 32); smaller M use its first rows."""
+    if shape not in _PROBLEMS_70B:
+        _PROBLEMS_70B.clear()   # keep at most one 70B weight set in host memory
+        K, N = shape
+        _PROBLEMS_70B[shape] = make_problem(32, K, N, frac=0.01,
+                                            seed=seed_for(3, SHAPES_70B.index(shape), 0))
+    p = _PROBLEMS_70B[shape]
+    return dataclasses.replace(p, M=M, X=np.ascontiguousarray(p.X[:M]))
+
+
+@pytest.mark.parametrize("shape", SHAPES_70B, ids=["qkv70", "o70", "gate_up70", "down70"])
+@pytest.mark.parametrize("M", [1, 32])
+def test_70b_full_size_sampled_columns(gpu_lib, shape, M):
+    """Llama-3-70B decode linears at full size (M = 1: gather mapping; M = 32:
+    two 16-row MFMA blocks); sampled columns against the oracle."""
+    K, N = shape
+    log(f"70B K={K} N={N} M={M}")
+    prob = _problem_70b(shape, M)
+    rng = np.random.default_rng(K + N + M)
+    cols = np.unique(np.concatenate([[0, 63, 64, N - 1], rng.choice(N, 128, replace=False)]))
+    y_ref = ref(prob, cols)
+    assert_bf16_close(run(gpu_lib, prob, "fused", "bf16")[:, cols], y_ref)
+    assert_f32_close(run(gpu_lib, prob, "fused", "f32")[:, cols], y_ref)
