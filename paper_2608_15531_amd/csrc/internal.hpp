@@ -9,7 +9,8 @@ namespace fqi {
 
 constexpr int kTileK = 128;     // K side of a dense/sparse tile = quantisation group
 constexpr int kTileN = 64;      // N side of a tile = one output strip
-constexpr int kMaxM = 32;       // rows the fused GEMV-regime kernel supports
+constexpr int kMaxM = 128;      // rows the kernels support
+constexpr int kSlabM = 32;      // rows one workgroup computes (two 16-row MFMA blocks)
 constexpr int kMaxBuckets = 256;
 constexpr int kXStride = 136;   // LDS row stride (elements) of a staged 128-wide X slice
 constexpr int kGatherMaxM = 1;  // up to this M the sparse path gathers X in LDS; above, MFMA
@@ -26,7 +27,9 @@ constexpr int kMaxStrips = int(kCounterRegion / 4);
 // Tile-COO exists.
 struct Plan {
   int M, K, N;
-  int MB;            // 16-row MFMA blocks: 1 (M <= 16) or 2 (M <= 32)
+  int MB;            // 16-row MFMA blocks per slab: 1 (M <= 16) or 2
+  int n_slabs;       // 32-row slabs of M, one workgroup set each
+  int slab_M;        // rows per slab: min(M, 32)
   int MODE;          // sparse mapping: 0 LDS gathers (M <= kGatherMaxM), 1 MFMA
   int n_strips;      // N / 64
   int T;             // tiles per strip, K / 128

@@ -71,6 +71,7 @@ struct MatmulArgs {
   int M, K, N;
   int y_f32;
   int T, S;
+  int n_slabs;         // 32-row slabs of M (grid = strips x splits x slabs)
   int slot_bytes;      // one wave's LDS slot
   int off_shc;         // per-wave sparse output buffers (gather mode)
   int off_flag;
@@ -326,7 +327,7 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
 }
 
 template <int MB, int MODE, bool DENSE, bool SPARSE, int NW>
-__global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs a) {
+__global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -337,10 +338,29 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs a) {
 
   // Workgroups are dealt round-robin to the eight XCDs; give each XCD a
   // contiguous run of (strip, split) pairs so the splits of one strip and
-  // neighbouring strips share an L2.
-  const int G = gridDim.x;
+  // neighbouring strips share an L2, and deal the row slabs of one (strip,
+  // split) to the same XCD one after another, so that all but the first read
+  // its weights from that L2.
+  const int G = gridDim.x / args.n_slabs;   // (strip, split) pairs
   const int bid = blockIdx.x;
-  const int logical = (G & 7) == 0 ? (bid & 7) * (G >> 3) + (bid >> 3) : bid;
+  int logical, slab;
+  if ((G & 7) == 0) {
+    const int t = bid >> 3;
+    slab = t % args.n_slabs;
+    logical = (bid & 7) * (G >> 3) + t / args.n_slabs;
+  } else {
+    slab = bid / G;
+    logical = bid - slab * G;
+  }
+  // This workgroup's rows [m0, m0 + M) as a problem of its own.
+  MatmulArgs a = args;
+  const int m0 = slab * fqi::kSlabM;
+  a.M = min(fqi::kSlabM, args.M - m0);
+  a.X = args.X + size_t(m0) * args.K;
+  a.Y = static_cast<char*>(args.Y) + size_t(m0) * args.N * (args.y_f32 ? 4 : 2);
+  if (args.y_addend) a.y_addend = args.y_addend + size_t(m0) * args.N;
+  a.partials = args.partials + size_t(slab) * (G / args.S) * args.S * fqi::kSlabM * 64;
+  a.counters = args.counters + size_t(slab) * (G / args.S);
   const int strip = logical / a.S;
   const int split = logical - strip * a.S;
   const int t_lo = int(int64_t(split) * a.T / a.S);
@@ -717,7 +737,7 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
                                        int(pl.lds_bytes));
     if (e != hipSuccess) return int(e);
   }
-  const unsigned grid = unsigned(pl.n_strips) * unsigned(pl.S);
+  const unsigned grid = unsigned(pl.n_strips) * unsigned(pl.S) * unsigned(pl.n_slabs);
   hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * NW), pl.lds_bytes, stream, args);
   return int(hipGetLastError());
 }
@@ -776,34 +796,40 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   p.M = M;
   p.K = K;
   p.N = N;
-  p.MB = M <= 16 ? 1 : 2;
+  p.n_slabs = (M + kSlabM - 1) / kSlabM;
+  p.slab_M = std::min(M, kSlabM);
+  p.MB = p.slab_M <= 16 ? 1 : 2;
   p.MODE = mode >= 0 ? mode : (M <= kGatherMaxM ? 0 : 1);
   // the gather mapping stages one 16-byte X chunk per lane: at most 4 rows
   if (p.MODE == 0 && M > kGatherLimitM) return false;
   p.n_strips = N / kTileN;
   p.T = K / kTileK;
+  // the grid policy counts every row slab's workgroups
   const bool eight = sparse && p.MODE == 1;
-  int S = split_k > 0 ? split_k : default_split(p.T, p.n_strips, eight);
+  const int units = p.n_strips * p.n_slabs;
+  int S = split_k > 0 ? split_k : default_split(p.T, units, eight);
   // each wave indexes its tiles' group offsets from one register: <= 63 tiles
   S = std::max(S, (p.T + 4 * 63 - 1) / (4 * 63));
   p.S = std::max(1, std::min(S, p.T));
-  p.NW = waves_per_workgroup(p.T, p.S, p.n_strips, eight);
+  p.NW = waves_per_workgroup(p.T, p.S, units, eight);
   p.B = sparse ? B : 1;
 
   if (p.MODE == 0) {
-    p.slot_bytes = align_up(size_t(M) * kXStride * 2, 16);
+    p.slot_bytes = align_up(size_t(p.slab_M) * kXStride * 2, 16);
   } else {
     p.slot_bytes = sparse ? kImageBytes : 0;   // 16 B-operand blocks of 64 x 16 B
   }
-  const size_t red_bytes = size_t(p.NW) * M * kTileN * 4;
+  const size_t red_bytes = size_t(p.NW) * p.slab_M * kTileN * 4;
   p.off_shc = align_up(std::max(p.NW * p.slot_bytes, red_bytes), 16);
-  const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * M * kTileN * 4 : 0;
+  const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * p.slab_M * kTileN * 4 : 0;
   p.off_flag = align_up(p.off_shc + shc_bytes, 16);
   p.off_trash = p.off_flag + 16;
   p.lds_bytes = p.off_trash + 16;
   if (p.lds_bytes > 160 * 1024) return false;
 
-  p.partial_bytes = p.S > 1 ? size_t(p.n_strips) * p.S * M * kTileN * 4 : 0;
+  // partial sums: [slab][strip][split][row][64] fp32, every slab kSlabM rows apart
+  p.partial_bytes = p.S > 1 ? size_t(p.n_slabs) * p.n_strips * p.S * kSlabM * kTileN * 4 : 0;
+  if (int64_t(p.n_slabs) * p.n_strips > kMaxStrips) return false;   // one counter each
   // every array is addressed with 32-bit byte offsets
   const size_t lim = size_t(1) << 31;
   if (size_t(K) * N / 2 >= lim || size_t(M) * K * 2 >= lim || p.partial_bytes >= lim) return false;
@@ -831,6 +857,7 @@ int launch_matmul(const Plan& pl, const MatmulPtrs& p, bool dense, bool sparse, 
   a.N = pl.N;
   a.T = pl.T;
   a.S = pl.S;
+  a.n_slabs = pl.n_slabs;
   a.slot_bytes = int(pl.slot_bytes);
   a.off_shc = int(pl.off_shc);
   a.off_flag = int(pl.off_flag);

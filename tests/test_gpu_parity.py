@@ -123,6 +123,11 @@ EXACT_CASES = [
     (8, 128, 64, 0.5, 0, c_params()),
     (2, 256, 64, 1.0, 0, c_params(buckets_per_tile=4)),
     (4, 512, 128, 0.0, 0, c_params()),
+    # more than 32 rows: 32-row slabs in the grid, ragged last slab, split-K
+    (33, 1024, 256, 0.02, 0, c_params()),
+    (64, 2048, 512, 0.01, 3, c_params()),
+    (100, 1024, 192, 0.03, 0, c_params(group_mode=1, buckets_per_tile=8)),
+    (128, 4096, 1024, 0.01, 0, c_params()),
 ]
 
 
@@ -300,3 +305,27 @@ def test_70b_full_size_sampled_columns(gpu_lib, shape, M):
     y_ref = ref(prob, cols)
     assert_bf16_close(run(gpu_lib, prob, "fused", "bf16")[:, cols], y_ref)
     assert_f32_close(run(gpu_lib, prob, "fused", "f32")[:, cols], y_ref)
+
+
+# ------------------------------------------------- up to 128 rows at full size --
+
+SHAPES_LARGE_M = [(4096, 14336), (14336, 4096)]
+
+
+@pytest.mark.parametrize("shape", SHAPES_LARGE_M, ids=["k4096_n14336", "k14336_n4096"])
+@pytest.mark.parametrize("M", [32, 64, 128])
+def test_large_m_full_size_sampled_columns(gpu_lib, shape, M):
+    """M = 32, 64, 128 on 4096 x 14336 and 14336 x 4096 (32-row slabs); sampled
+    columns against the oracle, every element against the unfused path."""
+    K, N = shape
+    log(f"large M K={K} N={N} M={M}")
+    prob = make_problem(M, K, N, frac=0.01,
+                        seed=seed_for(4, SHAPES_LARGE_M.index(shape), [32, 64, 128].index(M)))
+    rng = np.random.default_rng(K + N + M)
+    cols = np.unique(np.concatenate([[0, 63, 64, N - 1], rng.choice(N, 96, replace=False)]))
+    y_ref = ref(prob, cols)
+    assert_bf16_close(run(gpu_lib, prob, "fused", "bf16")[:, cols], y_ref)
+    y32 = run(gpu_lib, prob, "fused", "f32")
+    assert_f32_close(y32[:, cols], y_ref)
+    yu = run(gpu_lib, prob, "unfused", "f32")
+    assert np.linalg.norm(yu - y32) <= F32_FROB * np.linalg.norm(y32)

@@ -262,7 +262,7 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
 
 @pytest.mark.parametrize("kw,status", [
     (dict(M=0), "FQ_ERR_SHAPE"),
-    (dict(M=33), "FQ_ERR_UNSUPPORTED"),
+    (dict(M=129), "FQ_ERR_UNSUPPORTED"),
     (dict(K=1000), "FQ_ERR_SHAPE"),
     (dict(N=96), "FQ_ERR_SHAPE"),
     (dict(group_size=64), "FQ_ERR_UNSUPPORTED"),
@@ -272,7 +272,7 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
     (dict(flags=1, M=5), "FQ_ERR_UNSUPPORTED"),
     # 32-bit byte offsets: packed weights of 2^31 bytes, partial sums of 2^31 bytes
     (dict(K=131072, N=32768), "FQ_ERR_UNSUPPORTED"),
-    (dict(M=32, K=32768, N=65536, split_k=256), "FQ_ERR_UNSUPPORTED"),
+    (dict(M=128, K=32768, N=65536, split_k=64), "FQ_ERR_UNSUPPORTED"),
 ])
 def test_matmul_rejects_bad_problem(lib, kw, status):
     assert _call(lib, _problem(**kw)) == status
