@@ -161,6 +161,47 @@ fq_status fq_validate_tile_coo(int32_t K, int32_t N, const fq_tilecoo_params* p,
                                int64_t n_groups, const uint32_t* tile_indptr,
                                const uint16_t* bucket_info, const uint32_t* packed);
 
+/*
+ * fq_quantize_outlier_aware -- offline outlier-aware INT4 quantiser (host; the
+ * paper's offline preprocessing, Sec. 2.1 eq. 2-3 and Sec. 3).
+ *   W            fp32 [K][N] row-major, finite (FQ_ERR_RANGE otherwise).
+ *   group_size   quantisation group along K; K % group_size == 0, K % 8 == 0,
+ *                N % 8 == 0 (FQ_ERR_SHAPE otherwise).
+ *   outlier_frac in [0, 1]: the round(frac K N) weights of largest |w| (ties to
+ *                the lower row-major index; only weights whose bf16 value is
+ *                nonzero qualify) become bf16 outliers (round to nearest even).
+ * Every other weight is quantised per (group, column) by eq. 2 with the range
+ * [min(w_min, 0), max(w_max, 0)] of the group's non-outlier weights:
+ * s = smallest fp16 >= (w_max - w_min) / 15, z = clamp(round(-w_min / s), 0, 15),
+ * q = clamp(round(w / s) + z, 0, 15), rounding ties to even; an all-zero group
+ * gets s = 1, z = 0.  The code at an outlier position is the group's z, so
+ * dequant(W_Q) + W_O reproduces each outlier exactly in bf16.
+ * Outputs (caller-owned): Wq uint32 [K/8][N], scales fp16 bits [K/G][N],
+ * zeros uint32 [K/G][N/8] (layouts as for the matmul), and the outliers as
+ * (k_idx, n_idx, val) sorted by (k, n).  Two-call pattern: with Wq, scales,
+ * zeros, k_idx, n_idx and val all NULL only *nnz_out is computed.
+ */
+fq_status fq_quantize_outlier_aware(int32_t K, int32_t N, const float* W, int32_t group_size,
+                                    double outlier_frac, int64_t* nnz_out, uint32_t* Wq,
+                                    uint16_t* scales, uint32_t* zeros, int32_t* k_idx,
+                                    int32_t* n_idx, uint16_t* val);
+
+/*
+ * fq_fill_padding_slots -- stores original weights in Tile-COO padding slots
+ * (host; Sec. 3.2.1 notes that padding slots may carry original weight
+ * values).  For every padding slot (value bits 0) of a host Tile-COO whose
+ * tile-local position holds no real entry yet and whose weight W[k][n] has a
+ * nonzero bf16 value, the slot takes that value and the code of (k, n) in Wq
+ * becomes its group's zero-point, so the position is reproduced exactly.
+ * packed and Wq are updated in place; *n_filled receives the number of slots
+ * filled.  The Tile-COO is validated first (FQ_ERR_FORMAT), and stays valid.
+ */
+fq_status fq_fill_padding_slots(int32_t K, int32_t N, const float* W, int32_t group_size,
+                                const fq_tilecoo_params* p, int64_t n_groups,
+                                const uint32_t* tile_indptr, const uint16_t* bucket_info,
+                                uint32_t* packed, uint32_t* Wq, const uint32_t* zeros,
+                                int64_t* n_filled);
+
 /* Device-resident Tile-COO.  Pointers are device pointers owned by the caller;
  * n_groups and max_tile_groups come from fq_tilecoo_sizes. */
 typedef struct {

@@ -7,3 +7,4 @@ from .oracle import (  # noqa: F401
     dequant, f16_to_f64, matmul, matmul_tile_coo, outlier_part, pack_tile_coo,
     storage_bytes, unpack_tile_coo, zero_points,
 )
+from . import quant  # noqa: F401,E402

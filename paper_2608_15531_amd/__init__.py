@@ -98,6 +98,11 @@ _SIGS = {
     "fq_debug_decode_tile_coo": ([C.POINTER(fq_tilecoo_dev), C.c_int32, C.c_int32, _P, _P, _P,
                                   _P], C.c_int),
     "fq_status_string": ([C.c_int], C.c_char_p),
+    "fq_quantize_outlier_aware": ([C.c_int32, C.c_int32, _P, C.c_int32, C.c_double,
+                                   C.POINTER(C.c_int64), _P, _P, _P, _P, _P, _P], C.c_int),
+    "fq_fill_padding_slots": ([C.c_int32, C.c_int32, _P, C.c_int32,
+                               C.POINTER(fq_tilecoo_params), C.c_int64, _P, _P, _P, _P, _P,
+                               C.POINTER(C.c_int64)], C.c_int),
 }
 EXPORTS = tuple(_SIGS)
 
@@ -205,6 +210,57 @@ def fq_unpack_tile_coo(K: int, N: int, params, tile_indptr, bucket_info, packed)
                                   C.byref(nnz), k.ctypes.data, n.ctypes.data, v.ctypes.data),
            "fq_unpack_tile_coo")
     return k[:nnz.value], n[:nnz.value], v[:nnz.value]
+
+
+@dataclass
+class QuantizedWeight:
+    K: int
+    N: int
+    group: int
+    Wq: np.ndarray       # uint32 [K/8][N]
+    scales: np.ndarray   # uint16 [K/G][N] fp16 bits
+    zeros: np.ndarray    # uint32 [K/G][N/8]
+    k: np.ndarray        # int32 [nnz] outlier rows
+    n: np.ndarray        # int32 [nnz] outlier columns
+    v: np.ndarray        # uint16 [nnz] bf16 bits
+
+
+def fq_quantize_outlier_aware(W, outlier_frac: float, group: int = 128) -> QuantizedWeight:
+    """Split fp32 W [K][N] into INT4 W_Q (per-group affine) and bf16 outliers."""
+    lib = load()
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    K, N = W.shape
+    nnz = C.c_int64(0)
+    _check(lib.fq_quantize_outlier_aware(K, N, W.ctypes.data, group, float(outlier_frac),
+                                         C.byref(nnz), None, None, None, None, None, None),
+           "fq_quantize_outlier_aware")
+    Wq = np.empty((K // 8, N), np.uint32)
+    scales = np.empty((K // group, N), np.uint16)
+    zeros = np.empty((K // group, N // 8), np.uint32)
+    m = max(nnz.value, 1)
+    k, n, v = np.empty(m, np.int32), np.empty(m, np.int32), np.empty(m, np.uint16)
+    _check(lib.fq_quantize_outlier_aware(K, N, W.ctypes.data, group, float(outlier_frac),
+                                         C.byref(nnz), Wq.ctypes.data, scales.ctypes.data,
+                                         zeros.ctypes.data, k.ctypes.data, n.ctypes.data,
+                                         v.ctypes.data), "fq_quantize_outlier_aware")
+    c = nnz.value
+    return QuantizedWeight(K, N, group, Wq, scales, zeros, k[:c], n[:c], v[:c])
+
+
+def fq_fill_padding_slots(W, qw: QuantizedWeight, host: TileCOOHost) -> int:
+    """Store original weights in the padding slots of `host` (in place) and set
+    the matching codes of qw.Wq to their zero-points; returns the slots filled."""
+    lib = load()
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    K, N = W.shape
+    filled = C.c_int64(0)
+    pk = host.packed if host.packed.size else np.zeros(4, np.uint32)
+    _check(lib.fq_fill_padding_slots(K, N, W.ctypes.data, qw.group, C.byref(host.params),
+                                     int(host.sizes.n_groups), host.tile_indptr.ctypes.data,
+                                     host.bucket_info.ctypes.data, pk.ctypes.data,
+                                     qw.Wq.ctypes.data, qw.zeros.ctypes.data, C.byref(filled)),
+           "fq_fill_padding_slots")
+    return int(filled.value)
 
 
 # ---------------------------------------------------------------- device --

@@ -15,7 +15,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB_NAME = "libfq.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 
-HOST_SOURCES = ["capi.cpp", "tilecoo.cpp"]
+HOST_SOURCES = ["capi.cpp", "tilecoo.cpp", "quant.cpp"]
 HIP_SOURCES = ["kernels.hip"]
 
 # Packed-fp32 VALU forms are kept out of every HIP object.  MFMA results stay

@@ -12,6 +12,7 @@ from .gen import (  # noqa: F401
     WORKLOADS,
     bf16_bits_from_f32,
     make_activations,
+    make_dense_weight,
     make_exact_problem,
     make_problem,
     seed_for,

@@ -199,3 +199,11 @@ def make_activations(M: int, K: int, seed: int) -> np.ndarray:
     """bf16 bits of N(0,1) activations [M][K] (same recipe as make_problem's X)."""
     rng = np.random.Generator(np.random.PCG64(seed))
     return bf16_bits_from_f32(rng.standard_normal((M, K), dtype=np.float32))
+
+
+def make_dense_weight(K: int, N: int, seed: int = 0, df: float = 4.0,
+                      scale: float = 0.02) -> np.ndarray:
+    """Synthetic dense fp32 weight [K][N] for the quantiser: scale * Student-t(df),
+    heavy-tailed so that a small fraction of weights dominates the range."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return (scale * rng.standard_t(df, size=(K, N))).astype(np.float32)

@@ -329,3 +329,38 @@ def test_large_m_full_size_sampled_columns(gpu_lib, shape, M):
     assert_f32_close(y32[:, cols], y_ref)
     yu = run(gpu_lib, prob, "unfused", "f32")
     assert np.linalg.norm(yu - y32) <= F32_FROB * np.linalg.norm(y32)
+
+
+# ---------------------------------------------- quantiser -> fused kernel --
+
+@pytest.mark.parametrize("fill", [False, True], ids=["outliers", "outliers+padding"])
+def test_quantised_weight_through_fused_kernel(gpu_lib, fill):
+    """A synthetic dense weight quantised by the library (1 % outliers, padding
+    slots optionally filled with original weights) runs through the fused
+    kernel; parity against the oracle on the same quantised representation,
+    and the result approximates X W of the unquantised weight."""
+    from oracle import quant
+    from synth import make_activations, make_dense_weight
+    fq = gpu_lib
+    K, N, M = 4096, 4096, 8
+    W = make_dense_weight(K, N, seed=21)
+    qw = fq.fq_quantize_outlier_aware(W, 0.01)
+    host = fq.fq_pack_tile_coo(K, N, qw.k, qw.n, qw.v)
+    if fill:
+        assert fq.fq_fill_padding_slots(W, qw, host) > 0
+    k, n, v = fq.fq_unpack_tile_coo(K, N, host.params, host.tile_indptr, host.bucket_info,
+                                    host.packed)
+    X = make_activations(M, K, seed=22)
+    Xd = torch.from_numpy(X.view(np.int16).copy()).view(torch.bfloat16).cuda()
+    Wq = torch.from_numpy(qw.Wq.view(np.int32).copy()).cuda()
+    s = torch.from_numpy(qw.scales.view(np.int16).copy()).cuda()
+    z = torch.from_numpy(qw.zeros.view(np.int32).copy()).cuda()
+    Y = fq.fq_w4a16_outlier_matmul(Xd, Wq, s, z, fq.TileCOODevice(host), y_dtype="f32")
+    torch.cuda.synchronize()
+    y = Y.cpu().numpy()
+    y_ref = oracle.matmul(X, qw.Wq, qw.scales, qw.zeros, K, N, 128, k, n, v)
+    assert_f32_close(y, y_ref)
+    exact = oracle.bf16_to_f64(X) @ W.astype(np.float64)
+    rel = np.linalg.norm(y - exact) / np.linalg.norm(exact)
+    log(f"quantised fill={fill}: relative error of X W_hat against X W = {rel:.4f}")
+    assert rel < 0.1
