@@ -225,8 +225,9 @@ typedef struct {
  *   group_size  G, must be 128 (one group per 128 x 64 tile).
  *   y_dtype     FQ_Y_BF16 (round to nearest even once, after the full sum) or FQ_Y_F32.
  *   split_k     number of K ranges per 64-column strip; 0 lets the library choose.
- *   flags       0, or one FQ_SPARSE_* value to force the sparse-path mapping
- *               (the library otherwise picks by M).
+ *   flags       bit set: one FQ_SPARSE_* value in bits 0-1 to force the
+ *               sparse-path mapping (the library otherwise picks by M), and
+ *               the schedule switches FQ_SCHED_STREAM_K and FQ_FOUR_WAVES.
  */
 typedef struct {
   int32_t M;
@@ -242,7 +243,18 @@ typedef struct {
  * decodes one 16-byte group and gathers X[m][k] from LDS for every row (VALU dot2).
  * MFMA: the tile's outliers are scattered into an LDS image of the MFMA B
  * operand and multiplied on the matrix cores.  Both are exact in fp32. */
-enum { FQ_SPARSE_AUTO = 0, FQ_SPARSE_GATHER = 1, FQ_SPARSE_MFMA = 2 };
+enum { FQ_SPARSE_AUTO = 0, FQ_SPARSE_GATHER = 1, FQ_SPARSE_MFMA = 2, FQ_SPARSE_MASK = 3 };
+
+/* Schedule switches (fq_problem.flags), for ablation; the default is uniform
+ * split-K with the wave count the library picks.
+ *   FQ_SCHED_STREAM_K  with split_k == 0: Stream-K (Sec. 3.1) -- one workgroup
+ *                      per resident slot, each taking an even share of the
+ *                      (strip, tile) iteration space, processed as per-strip
+ *                      segments; strips shared by several workgroups are
+ *                      summed by the last to arrive, in workgroup order.
+ *   FQ_FOUR_WAVES      never run eight waves per workgroup (the extra waves
+ *                      that overlap the outlier work with the dense work). */
+enum { FQ_SCHED_STREAM_K = 4, FQ_FOUR_WAVES = 8 };
 
 /*
  * fq_workspace_bytes -- device workspace the matmul entry points need for

@@ -34,6 +34,8 @@ FQ_SPARSE_AUTO = 0
 FQ_SPARSE_GATHER = 1
 FQ_SPARSE_MFMA = 2
 _SPARSE_MODES = {"auto": FQ_SPARSE_AUTO, "gather": FQ_SPARSE_GATHER, "mfma": FQ_SPARSE_MFMA}
+FQ_SCHED_STREAM_K = 4
+FQ_FOUR_WAVES = 8
 
 
 class FqError(RuntimeError):
@@ -315,8 +317,8 @@ def workspace(nbytes: int, device, stream_handle: int):
     return buf
 
 
-def _problem(M, K, N, y_dtype, split_k, group=128, sparse="auto") -> fq_problem:
-    return fq_problem(M, K, N, group, y_dtype, split_k, _SPARSE_MODES[sparse])
+def _problem(M, K, N, y_dtype, split_k, group=128, sparse="auto", flags=0) -> fq_problem:
+    return fq_problem(M, K, N, group, y_dtype, split_k, _SPARSE_MODES[sparse] | flags)
 
 
 def _check_tensor(t, dtype, shape, name):
@@ -347,11 +349,12 @@ def _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group):
 
 def fq_w4a16_outlier_matmul(X, Wq, scales, zeros, tc: TileCOODevice, Y=None, y_dtype="bf16",
                             split_k: int = 0, stream=None, ws=None, group: int = 128,
-                            sparse: str = "auto"):
-    """Fused Y = X dequant(W_Q) + X W_O on the GPU; returns Y."""
+                            sparse: str = "auto", flags: int = 0):
+    """Fused Y = X dequant(W_Q) + X W_O on the GPU; returns Y.  flags: any of
+    FQ_SCHED_STREAM_K, FQ_FOUR_WAVES."""
     lib = load()
     M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
-    pr = _problem(M, K, N, ydt, split_k, group, sparse)
+    pr = _problem(M, K, N, ydt, split_k, group, sparse, flags)
     need = C.c_size_t(0)
     _check(lib.fq_workspace_bytes(C.byref(pr), C.byref(need)), "fq_workspace_bytes")
     sh = _stream_handle(stream, X.device)
@@ -367,11 +370,11 @@ def fq_w4a16_outlier_matmul(X, Wq, scales, zeros, tc: TileCOODevice, Y=None, y_d
 
 def fq_w4a16_outlier_matmul_unfused(X, Wq, scales, zeros, tc: TileCOODevice, Y=None,
                                     y_dtype="bf16", split_k: int = 0, stream=None, ws=None,
-                                    group: int = 128, sparse: str = "auto"):
+                                    group: int = 128, sparse: str = "auto", flags: int = 0):
     """Two-kernel baseline (dense W4A16 then Tile-COO SpMM); returns Y."""
     lib = load()
     M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
-    pr = _problem(M, K, N, ydt, split_k, group, sparse)
+    pr = _problem(M, K, N, ydt, split_k, group, sparse, flags)
     need = C.c_size_t(0)
     _check(lib.fq_workspace_bytes_unfused(C.byref(pr), C.byref(need)),
            "fq_workspace_bytes_unfused")
@@ -388,11 +391,11 @@ def fq_w4a16_outlier_matmul_unfused(X, Wq, scales, zeros, tc: TileCOODevice, Y=N
 
 
 def fq_w4a16_matmul(X, Wq, scales, zeros, Y=None, y_dtype="bf16", split_k: int = 0,
-                    stream=None, ws=None, group: int = 128):
+                    stream=None, ws=None, group: int = 128, flags: int = 0):
     """Dense-only Y = X dequant(W_Q) (outliers ignored); returns Y."""
     lib = load()
     M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
-    pr = _problem(M, K, N, ydt, split_k, group)
+    pr = _problem(M, K, N, ydt, split_k, group, flags=flags)
     need = C.c_size_t(0)
     _check(lib.fq_workspace_bytes(C.byref(pr), C.byref(need)), "fq_workspace_bytes")
     sh = _stream_handle(stream, X.device)
@@ -421,9 +424,9 @@ def fq_debug_decode_tile_coo(tc: TileCOODevice, K: int, N: int, stream=None):
 
 
 def fq_workspace_bytes(M: int, K: int, N: int, y_dtype=FQ_Y_BF16, split_k: int = 0,
-                       group: int = 128) -> int:
+                       group: int = 128, flags: int = 0) -> int:
     lib = load()
-    pr = _problem(M, K, N, y_dtype, split_k, group)
+    pr = _problem(M, K, N, y_dtype, split_k, group, flags=flags)
     need = C.c_size_t(0)
     _check(lib.fq_workspace_bytes(C.byref(pr), C.byref(need)), "fq_workspace_bytes")
     return need.value

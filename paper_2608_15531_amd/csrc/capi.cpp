@@ -16,8 +16,10 @@ fq_status check_problem(const fq_problem* pr) {
   if (pr->group_size != fqi::kTileK) return FQ_ERR_UNSUPPORTED;
   if (pr->M > fqi::kMaxM) return FQ_ERR_UNSUPPORTED;
   if (pr->y_dtype != FQ_Y_BF16 && pr->y_dtype != FQ_Y_F32) return FQ_ERR_UNSUPPORTED;
-  if (pr->flags < FQ_SPARSE_AUTO || pr->flags > FQ_SPARSE_MFMA) return FQ_ERR_UNSUPPORTED;
-  if (pr->flags == FQ_SPARSE_GATHER && pr->M > fqi::kGatherLimitM) return FQ_ERR_UNSUPPORTED;
+  if (pr->flags & ~(FQ_SPARSE_MASK | FQ_SCHED_STREAM_K | FQ_FOUR_WAVES)) return FQ_ERR_UNSUPPORTED;
+  const int mapping = pr->flags & FQ_SPARSE_MASK;
+  if (mapping > FQ_SPARSE_MFMA) return FQ_ERR_UNSUPPORTED;
+  if (mapping == FQ_SPARSE_GATHER && pr->M > fqi::kGatherLimitM) return FQ_ERR_UNSUPPORTED;
   return FQ_OK;
 }
 
@@ -45,15 +47,18 @@ fq_status check_tc(const fq_problem* pr, const fq_tilecoo_dev* tc) {
   return FQ_OK;
 }
 
+int plan_opts(const fq_problem* pr);
+
 fq_status run(const fq_problem* pr, const uint16_t* X, const uint32_t* Wq,
               const uint16_t* scales, const uint32_t* zeros, const fq_tilecoo_dev* tc, void* Y,
               void* workspace, size_t workspace_bytes, void* stream, bool dense, bool sparse,
               const float* y_addend) {
   fqi::Plan plan;
-  const int mode = pr->flags == FQ_SPARSE_GATHER ? 0 : pr->flags == FQ_SPARSE_MFMA ? 1 : -1;
+  const int mapping = pr->flags & FQ_SPARSE_MASK;
+  const int mode = mapping == FQ_SPARSE_GATHER ? 0 : mapping == FQ_SPARSE_MFMA ? 1 : -1;
   if (!fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, dense, sparse,
                       sparse ? tc->params.buckets_per_tile : 0,
-                      sparse ? tc->max_tile_groups : 0, &plan, mode))
+                      sparse ? tc->max_tile_groups : 0, &plan, mode, plan_opts(pr)))
     return FQ_ERR_UNSUPPORTED;
   if (!workspace) return FQ_ERR_WORKSPACE;
   if (workspace_bytes < plan.ws_bytes || !aligned(workspace, 256)) return FQ_ERR_WORKSPACE;
@@ -76,6 +81,11 @@ fq_status run(const fq_problem* pr, const uint16_t* X, const uint32_t* Wq,
 }
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+int plan_opts(const fq_problem* pr) {
+  return ((pr->flags & FQ_SCHED_STREAM_K) ? fqi::kOptStreamK : 0) |
+         ((pr->flags & FQ_FOUR_WAVES) ? fqi::kOptFourWaves : 0);
+}
 
 }  // namespace
 
@@ -109,7 +119,8 @@ fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes) {
   bool any = false;
   for (int mode = -1; mode <= 1; ++mode) {
     for (int sparse = 0; sparse <= 1; ++sparse) {
-      if (fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, true, sparse != 0, 1, 0, &pl, mode)) {
+      if (fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, true, sparse != 0, 1, 0, &pl, mode,
+                         plan_opts(pr))) {
         any = true;
         need = pl.ws_bytes > need ? pl.ws_bytes : need;
       }

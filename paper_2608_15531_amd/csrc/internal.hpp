@@ -33,8 +33,11 @@ struct Plan {
   int MODE;          // sparse mapping: 0 LDS gathers (M <= kGatherMaxM), 1 MFMA
   int n_strips;      // N / 64
   int T;             // tiles per strip, K / 128
-  int S;             // K ranges per strip (split-K)
+  int S;             // K ranges per strip (explicit split-K); 1 under Stream-K
   int NW;            // waves per workgroup: 4 or 8
+  int stream;        // 1: Stream-K schedule, 0: uniform split-K
+  int G;             // workgroups per slab
+  int C;             // partial-sum slots per strip (most contributors to one strip)
   int B;             // buckets per tile
   // dynamic LDS layout, bytes: four wave slots (X slice or B-operand image),
   // then the gather-mode sparse output buffers
@@ -43,10 +46,14 @@ struct Plan {
   size_t partial_bytes, ws_bytes;
 };
 
+// Schedule options of make_plan (bit set).
+constexpr int kOptStreamK = 1;     // Stream-K ranges instead of uniform split-K (split_k == 0)
+constexpr int kOptFourWaves = 2;   // never eight waves per workgroup
+
 // Returns false when (M, K, N) is outside what the kernels implement.
 // mode: -1 picks the sparse mapping by M, 0 forces gathers, 1 forces MFMA.
 bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
-               int64_t max_tile_groups, Plan* plan, int mode = -1);
+               int64_t max_tile_groups, Plan* plan, int mode = -1, int opts = 0);
 
 struct MatmulPtrs {
   const uint16_t* X;

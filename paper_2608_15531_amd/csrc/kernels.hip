@@ -71,7 +71,9 @@ struct MatmulArgs {
   int M, K, N;
   int y_f32;
   int T, S;
-  int n_slabs;         // 32-row slabs of M (grid = strips x splits x slabs)
+  int stream;          // 1: Stream-K ranges; 0: S uniform splits per strip
+  int C;               // partial-sum slots per strip (most contributors to one strip)
+  int n_slabs;         // 32-row slabs of M (grid = workgroups per slab x slabs)
   int slot_bytes;      // one wave's LDS slot
   int off_shc;         // per-wave sparse output buffers (gather mode)
   int off_flag;
@@ -326,7 +328,7 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
   for (int j = 0; j < 4; ++j) lds_store16(addr[j], 0u);
 }
 
-template <int MB, int MODE, bool DENSE, bool SPARSE, int NW>
+template <int MB, int MODE, bool DENSE, bool SPARSE, int NW, bool SK>
 __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
@@ -336,40 +338,46 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   const int h = lane >> 4;                     // k-chunk of the MFMA operands
   const int c4 = lane & 15;                    // MFMA column / A row
 
-  // Workgroups are dealt round-robin to the eight XCDs; give each XCD a
-  // contiguous run of (strip, split) pairs so the splits of one strip and
-  // neighbouring strips share an L2, and deal the row slabs of one (strip,
-  // split) to the same XCD one after another, so that all but the first read
-  // its weights from that L2.
-  const int G = gridDim.x / args.n_slabs;   // (strip, split) pairs
+  // Work: the units (strip, tile) of each 32-row slab, strip-major
+  // (u = strip * T + tile, which is also the Tile-COO tile index).  A
+  // workgroup takes a contiguous range of units -- one (strip, K range) under
+  // plain split-K, or an even share of all units under Stream-K (Sec. 3.1),
+  // which may span strip boundaries -- and processes it as segments that each
+  // lie in one strip.  Workgroups are dealt round-robin to the eight XCDs;
+  // give each XCD a contiguous run of workgroups so that neighbouring ranges
+  // share an L2, and deal the row slabs of one range to the same XCD one after
+  // another, so that all but the first read its weights from that L2.
+  const int G = gridDim.x / args.n_slabs;   // workgroups per slab
   const int bid = blockIdx.x;
-  int logical, slab;
+  int wg, slab;
   if ((G & 7) == 0) {
     const int t = bid >> 3;
     slab = t % args.n_slabs;
-    logical = (bid & 7) * (G >> 3) + t / args.n_slabs;
+    wg = (bid & 7) * (G >> 3) + t / args.n_slabs;
   } else {
     slab = bid / G;
-    logical = bid - slab * G;
+    wg = bid - slab * G;
   }
   // This workgroup's rows [m0, m0 + M) as a problem of its own.
   MatmulArgs a = args;
   const int m0 = slab * fqi::kSlabM;
+  const int n_strips = args.N / 64;
   a.M = min(fqi::kSlabM, args.M - m0);
   a.X = args.X + size_t(m0) * args.K;
   a.Y = static_cast<char*>(args.Y) + size_t(m0) * args.N * (args.y_f32 ? 4 : 2);
   if (args.y_addend) a.y_addend = args.y_addend + size_t(m0) * args.N;
-  a.partials = args.partials + size_t(slab) * (G / args.S) * args.S * fqi::kSlabM * 64;
-  a.counters = args.counters + size_t(slab) * (G / args.S);
-  const int strip = logical / a.S;
-  const int split = logical - strip * a.S;
-  const int t_lo = int(int64_t(split) * a.T / a.S);
-  const int t_hi = int(int64_t(split + 1) * a.T / a.S);
-  const int nt = t_hi - t_lo;
-  const int w_lo = t_lo + (nt * wave) / NW;    // this wave's tiles [w_lo, w_hi)
-  const int w_hi = t_lo + (nt * (wave + 1)) / NW;
-  const int n0 = strip * 64;
-  const int64_t tile_base = int64_t(strip) * a.T;
+  a.partials = args.partials + size_t(slab) * n_strips * args.C * fqi::kSlabM * 64;
+  a.counters = args.counters + size_t(slab) * n_strips;
+  const int64_t U = int64_t(n_strips) * a.T;
+  int64_t u_begin, u_end;
+  if (SK) {
+    u_begin = int64_t(wg) * U / G;
+    u_end = int64_t(wg + 1) * U / G;
+  } else {
+    const int st = wg / a.S, sp = wg - st * a.S;
+    u_begin = int64_t(st) * a.T + int64_t(sp) * a.T / a.S;
+    u_end = int64_t(st) * a.T + int64_t(sp + 1) * a.T / a.S;
+  }
 
   unsigned char* slot = smem + size_t(wave) * a.slot_bytes;
   uint16_t* xs = reinterpret_cast<uint16_t*>(slot);   // MODE 0: X slice
@@ -380,27 +388,8 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   float* shc_all = reinterpret_cast<float*>(smem + a.off_shc);
   float* shc = shc_all + size_t(wave) * a.M * 64;
   int* flag = reinterpret_cast<int*>(smem + a.off_flag);
+  float* red = reinterpret_cast<float*>(smem);   // reuses the wave slots
 
-  if (SPARSE && MODE == 0)
-    for (int i = lane; i < a.M * 64; i += 64) shc[i] = 0.f;
-  if (SPARSE && MODE == 1) {
-    uint4* b4 = reinterpret_cast<uint4*>(bo);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) b4[i * 64 + lane] = uint4{0u, 0u, 0u, 0u};
-  }
-
-  // Group offsets of this wave's tiles: lane i holds tile_indptr[w_lo + i].
-  // The value is used raw (clamped only when read) so that nothing waits for
-  // it before the first tiles' dense loads are out.
-  uint32_t tp = 0;
-  if (SPARSE && lane <= w_hi - w_lo) tp = a.tile_indptr[tile_base + w_lo + lane];
-  __builtin_amdgcn_wave_barrier();
-
-  f32x4_t acc[MB][4];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) acc[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const bf16x8_t ones = __builtin_bit_cast(
       bf16x8_t, u32x4_t{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
 
@@ -423,6 +412,13 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   }
   const uint32_t img = lds_address(bo);                  // this wave's image
   const uint32_t trash = lds_address(smem + a.off_trash);
+
+
+  // The current segment (read by the lambdas below).
+  int strip = 0, n0 = 0, w_lo = 0, w_hi = 0;
+  int64_t tile_base = 0;
+  uint32_t tp = 0;
+  f32x4_t acc[MB][4];
 
   auto issue_sparse = [&](int t, TileRegs<MB, MODE>& r) __attribute__((always_inline)) {
     uint32_t g0 = 0, g1 = 0;
@@ -572,134 +568,180 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
     __builtin_amdgcn_wave_barrier();
   };
 
-  // D register buffers, all in flight: while tile t is computed from one,
-  // the loads of tiles t+1 .. t+D-1 fill the others; when t is done its
-  // buffer is refilled with tile t+D.  Every issue is unconditional (past the
-  // wave's last tile it re-reads that tile, which is still in cache), so each
-  // wait is exact: waiting for tile t leaves the (D-1) NL loads of the
-  // following tiles in flight.  The loop body handles D tiles and has a
-  // single back edge, so the compiler's own load tracking sees the same order
-  // on every entry; sched_barrier keeps the scheduler from sinking a tile's
-  // loads below the next wait, which would cut the prefetch depth.
-  constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
-  constexpr int D = pipeline_depth<MB>();
-  TileRegs<MB, MODE> rg[D];
-  if (w_lo < w_hi) {
-    const int last = w_hi - 1;
-    // The first tiles' dense loads go out before the group offsets have
-    // arrived; only the group loads wait for them.
-#pragma unroll
-    for (int i = 0; i < D; ++i) {
-      load_tile_dense<MB, MODE, DENSE>(a, op, min(w_lo + i, last), n0, rg[i]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int i = 0; i < D; ++i) {
-      issue_sparse(min(w_lo + i, last), rg[i]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    auto round = [&](int t) __attribute__((always_inline)) {
-#pragma unroll
-      for (int i = 0; i < D; ++i) {
-        wait_vmcnt<(D - 1) * NL>();
-        compute(rg[i]);
-        issue(min(t + i + D, last), rg[i]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    };
-    // The first round is peeled and the loop nested in it: the prologue's
-    // load order (all dense loads, then all group loads) differs from the
-    // steady state's, and the loop header must only be reached in the latter.
-    int t = w_lo;
-    if (t + D - 1 < w_hi) {
-      round(t);
-      for (t += D; t + D - 1 < w_hi; t += D) round(t);
-    }
-    // fewer than D tiles left, all already loaded: no further issue
-    static_for<0, D - 1>([&](auto ic) {
-      constexpr int i = decltype(ic)::value;
-      if (t + i < w_hi) {
-        wait_vmcnt<(D - 2 - i) * NL>();
-        compute(rg[i]);
-      }
-    });
-  }
-  __syncthreads();
 
-  // ---------------------------------------------------------------- reduce
-  float* red = reinterpret_cast<float*>(smem);   // reuses the wave slots
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = mb * 16 + 4 * h + r;
-      if (row < a.M)
-        *reinterpret_cast<f32x4_t*>(red + (wave * a.M + row) * 64 + 4 * c4) =
-            f32x4_t{acc[mb][0][r], acc[mb][1][r], acc[mb][2][r], acc[mb][3][r]};
-    }
-  __syncthreads();
-
-  const bool split_k = a.S > 1;
   // Partial sums cross workgroups through device-coherent (sc1) 16-byte
   // accesses, the encoding of relaxed agent-scope atomics; no cache-wide
   // writeback or invalidate is issued.
   const __amdgpu_buffer_rsrc_t prs =
-      make_rsrc(a.partials, uint32_t(a.N) * uint32_t(a.S) * uint32_t(a.M) * 4u);
-  const uint32_t strip_part = uint32_t(strip) * uint32_t(a.S) * uint32_t(a.M) * 256u;  // bytes
-  for (int i = tid; i < a.M * 16; i += 64 * NW) {
-    const int m = i >> 4;
-    const int cq = i & 15;
-    f32x4_t v{0.f, 0.f, 0.f, 0.f};
+      make_rsrc(a.partials, uint32_t(n_strips) * uint32_t(a.C) * uint32_t(a.M) * 256u);
+
+  for (int64_t u = u_begin; u < u_end;) {
+    // ------------------------------------------------------------ segment
+    strip = int(u / a.T);
+    const int t_lo = int(u - int64_t(strip) * a.T);
+    const int t_hi = int(min(int64_t(a.T), int64_t(t_lo) + (u_end - u)));
+    u += t_hi - t_lo;
+    // contributors to this strip, and this workgroup's place among them
+    int n_contrib, my_slot;
+    if (SK) {
+      const int64_t first = ((int64_t(strip) * a.T + 1) * G - 1) / U;
+      const int64_t last = (int64_t(strip + 1) * a.T * G - 1) / U;
+      n_contrib = int(last - first + 1);
+      my_slot = int(wg - first);
+    } else {
+      n_contrib = a.S;
+      my_slot = wg - (wg / a.S) * a.S;
+    }
+    const int nt = t_hi - t_lo;
+    w_lo = t_lo + (nt * wave) / NW;    // this wave's tiles [w_lo, w_hi)
+    w_hi = t_lo + (nt * (wave + 1)) / NW;
+    n0 = strip * 64;
+    tile_base = int64_t(strip) * a.T;
+
+    if (SPARSE && MODE == 0)
+      for (int i = lane; i < a.M * 64; i += 64) shc[i] = 0.f;
+    if (SPARSE && MODE == 1) {
+      uint4* b4 = reinterpret_cast<uint4*>(bo);
 #pragma unroll
-    for (int w = 0; w < NW; ++w)
-      v += *reinterpret_cast<const f32x4_t*>(red + (w * a.M + m) * 64 + 4 * cq);
-    if (SPARSE && MODE == 0) {
+      for (int i = 0; i < 16; ++i) b4[i * 64 + lane] = uint4{0u, 0u, 0u, 0u};
+    }
+    // Group offsets of this wave's tiles: lane i holds tile_indptr[w_lo + i].
+    // The value is used raw (clamped only when read) so that nothing waits
+    // for it before the first tiles' dense loads are out.
+    tp = 0;
+    if (SPARSE && lane <= w_hi - w_lo) tp = a.tile_indptr[tile_base + w_lo + lane];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // D register buffers, all in flight: while tile t is computed from one,
+    // the loads of tiles t+1 .. t+D-1 fill the others; when t is done its
+    // buffer is refilled with tile t+D.  Every issue is unconditional (past the
+    // wave's last tile it re-reads that tile, which is still in cache), so each
+    // wait is exact: waiting for tile t leaves the (D-1) NL loads of the
+    // following tiles in flight.  The loop body handles D tiles and has a
+    // single back edge, so the compiler's own load tracking sees the same order
+    // on every entry; sched_barrier keeps the scheduler from sinking a tile's
+    // loads below the next wait, which would cut the prefetch depth.
+    constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
+    constexpr int D = pipeline_depth<MB>();
+    TileRegs<MB, MODE> rg[D];
+    if (w_lo < w_hi) {
+      const int last = w_hi - 1;
+      // The first tiles' dense loads go out before the group offsets have
+      // arrived; only the group loads wait for them.
+  #pragma unroll
+      for (int i = 0; i < D; ++i) {
+        load_tile_dense<MB, MODE, DENSE>(a, op, min(w_lo + i, last), n0, rg[i]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  #pragma unroll
+      for (int i = 0; i < D; ++i) {
+        issue_sparse(min(w_lo + i, last), rg[i]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      auto round = [&](int t) __attribute__((always_inline)) {
+  #pragma unroll
+        for (int i = 0; i < D; ++i) {
+          wait_vmcnt<(D - 1) * NL>();
+          compute(rg[i]);
+          issue(min(t + i + D, last), rg[i]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      };
+      // The first round is peeled and the loop nested in it: the prologue's
+      // load order (all dense loads, then all group loads) differs from the
+      // steady state's, and the loop header must only be reached in the latter.
+      int t = w_lo;
+      if (t + D - 1 < w_hi) {
+        round(t);
+        for (t += D; t + D - 1 < w_hi; t += D) round(t);
+      }
+      // fewer than D tiles left, all already loaded: no further issue
+      static_for<0, D - 1>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        if (t + i < w_hi) {
+          wait_vmcnt<(D - 2 - i) * NL>();
+          compute(rg[i]);
+        }
+      });
+    }
+    __syncthreads();
+
+    // -------------------------------------------------------------- reduce
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = mb * 16 + 4 * h + r;
+        if (row < a.M)
+          *reinterpret_cast<f32x4_t*>(red + (wave * a.M + row) * 64 + 4 * c4) =
+              f32x4_t{acc[mb][0][r], acc[mb][1][r], acc[mb][2][r], acc[mb][3][r]};
+      }
+    __syncthreads();
+
+    const bool shared = n_contrib > 1;
+    const uint32_t strip_part = uint32_t(strip) * uint32_t(a.C) * uint32_t(a.M) * 256u;  // bytes
+    for (int i = tid; i < a.M * 16; i += 64 * NW) {
+      const int m = i >> 4;
+      const int cq = i & 15;
+      f32x4_t v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int w = 0; w < NW; ++w)
-        v += *reinterpret_cast<const f32x4_t*>(shc_all + (w * a.M + m) * 64 + 4 * cq);
-    }
-    if (split_k) {
-      const uint32_t off = strip_part + uint32_t(split * a.M + m) * 256u + uint32_t(cq) * 16u;
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), prs, int(off), 0, kSc1);
-    } else {
-      store_out(a, m, n0 + 4 * cq, v);
-    }
-  }
-  if (split_k) {
-    __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores have completed
-    __syncthreads();
-    if (tid == 0) {
-      const uint32_t old =
-          __hip_atomic_fetch_add(a.counters + strip, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      *flag = (old == uint32_t(a.S - 1));
-    }
-    __syncthreads();
-    if (*flag) {
-      // The last workgroup of the strip adds the partials in split order,
-      // with up to eight loads in flight per thread.
-      constexpr int kBatch = 8;
-      for (int i = tid; i < a.M * 16; i += 64 * NW) {
-        const int m = i >> 4;
-        const int cq = i & 15;
-        const uint32_t base = strip_part + uint32_t(m) * 256u + uint32_t(cq) * 16u;
-        const uint32_t split_stride = uint32_t(a.M) * 256u;
-        f32x4_t v{0.f, 0.f, 0.f, 0.f};
-        for (int s0 = 0; s0 < a.S; s0 += kBatch) {
-          u32x4_t part[kBatch];
+        v += *reinterpret_cast<const f32x4_t*>(red + (w * a.M + m) * 64 + 4 * cq);
+      if (SPARSE && MODE == 0) {
 #pragma unroll
-          for (int j = 0; j < kBatch; ++j) {
-            const int sp = min(s0 + j, a.S - 1);   // in range; surplus loads unused
-            part[j] = __builtin_amdgcn_raw_buffer_load_b128(prs, int(base + uint32_t(sp) * split_stride), 0, kSc1);
-          }
-#pragma unroll
-          for (int j = 0; j < kBatch; ++j)
-            if (s0 + j < a.S) v += __builtin_bit_cast(f32x4_t, part[j]);
-        }
+        for (int w = 0; w < NW; ++w)
+          v += *reinterpret_cast<const f32x4_t*>(shc_all + (w * a.M + m) * 64 + 4 * cq);
+      }
+      if (shared) {
+        const uint32_t off = strip_part + uint32_t(my_slot * a.M + m) * 256u + uint32_t(cq) * 16u;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), prs, int(off), 0, kSc1);
+      } else {
         store_out(a, m, n0 + 4 * cq, v);
       }
-      if (tid == 0)
-        __hip_atomic_store(a.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    if (shared) {
+      __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores have completed
+      __syncthreads();
+      if (tid == 0) {
+        const uint32_t old =
+            __hip_atomic_fetch_add(a.counters + strip, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *flag = (old == uint32_t(n_contrib - 1));
+      }
+      __syncthreads();
+      if (*flag) {
+        // The last contributor adds the partials in contributor order, with
+        // up to eight loads in flight per thread.
+        constexpr int kBatch = 8;
+        for (int i = tid; i < a.M * 16; i += 64 * NW) {
+          const int m = i >> 4;
+          const int cq = i & 15;
+          const uint32_t base = strip_part + uint32_t(m) * 256u + uint32_t(cq) * 16u;
+          const uint32_t slot_stride = uint32_t(a.M) * 256u;
+          f32x4_t v{0.f, 0.f, 0.f, 0.f};
+          for (int s0 = 0; s0 < n_contrib; s0 += kBatch) {
+            u32x4_t part[kBatch];
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j) {
+              const int sp = min(s0 + j, n_contrib - 1);   // in range; surplus loads unused
+              part[j] = __builtin_amdgcn_raw_buffer_load_b128(prs, int(base + uint32_t(sp) * slot_stride), 0, kSc1);
+            }
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j)
+              if (s0 + j < n_contrib) v += __builtin_bit_cast(f32x4_t, part[j]);
+          }
+          store_out(a, m, n0 + 4 * cq, v);
+        }
+        if (tid == 0)
+          __hip_atomic_store(a.counters + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    // Under split-K the range lies in one strip: a single segment.
+    if (!SK) break;
+    __syncthreads();   // the next segment reuses LDS
   }
 }
 
@@ -728,25 +770,31 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
   }
 }
 
-template <int MB, int MODE, bool DENSE, bool SPARSE, int NW>
+template <int MB, int MODE, bool DENSE, bool SPARSE, int NW, bool SK>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, MODE, DENSE, SPARSE, NW>;
+  auto kern = matmul_kernel<MB, MODE, DENSE, SPARSE, NW, SK>;
   if (pl.lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        int(pl.lds_bytes));
     if (e != hipSuccess) return int(e);
   }
-  const unsigned grid = unsigned(pl.n_strips) * unsigned(pl.S) * unsigned(pl.n_slabs);
+  const unsigned grid = unsigned(pl.G) * unsigned(pl.n_slabs);
   hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * NW), pl.lds_bytes, stream, args);
   return int(hipGetLastError());
 }
 
+template <int MB, int MODE, int NW, bool SK>
+int launch_sched(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
+  if (dense && sparse) return launch_variant<MB, MODE, true, true, NW, SK>(pl, a, s);
+  if (dense) return launch_variant<MB, MODE, true, false, NW, SK>(pl, a, s);
+  return launch_variant<MB, MODE, false, true, NW, SK>(pl, a, s);
+}
+
 template <int MB, int MODE, int NW>
 int launch_waves(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
-  if (dense && sparse) return launch_variant<MB, MODE, true, true, NW>(pl, a, s);
-  if (dense) return launch_variant<MB, MODE, true, false, NW>(pl, a, s);
-  return launch_variant<MB, MODE, false, true, NW>(pl, a, s);
+  return pl.stream ? launch_sched<MB, MODE, NW, true>(pl, a, dense, sparse, s)
+                   : launch_sched<MB, MODE, NW, false>(pl, a, dense, sparse, s);
 }
 
 template <int MB, int MODE>
@@ -762,9 +810,9 @@ namespace fqi {
 namespace {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Grid shape.  The fused kernel with the MFMA outlier mapping is bound by
-// per-SIMD issue (dequantisation VALU, MFMA and the LDS image of the
-// outliers), so when the strips fit the CUs it runs eight waves per
+// Grid shape under split-K.  The fused kernel with the MFMA outlier mapping
+// is bound by per-SIMD issue (dequantisation VALU, MFMA and the LDS image of
+// the outliers), so when the strips fit the CUs it runs eight waves per
 // workgroup -- two per SIMD, overlapping one another's VALU, MFMA and LDS
 // work -- with the largest split that keeps at most one workgroup per CU
 // and one tile per wave.  Otherwise (dense only, the gather mapping, or more
@@ -787,7 +835,7 @@ int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
 }  // namespace
 
 bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
-               int64_t max_tile_groups, Plan* pl, int mode) {
+               int64_t max_tile_groups, Plan* pl, int mode, int opts) {
   (void)max_tile_groups;
   if (M < 1 || M > kMaxM || K < kTileK || N < kTileN || K % kTileK || N % kTileN) return false;
   if (N / kTileN > kMaxStrips) return false;
@@ -805,13 +853,44 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   p.n_strips = N / kTileN;
   p.T = K / kTileK;
   // the grid policy counts every row slab's workgroups
-  const bool eight = sparse && p.MODE == 1;
+  const bool eight = sparse && p.MODE == 1 && !(opts & kOptFourWaves);
   const int units = p.n_strips * p.n_slabs;
-  int S = split_k > 0 ? split_k : default_split(p.T, units, eight);
-  // each wave indexes its tiles' group offsets from one register: <= 63 tiles
-  S = std::max(S, (p.T + 4 * 63 - 1) / (4 * 63));
-  p.S = std::max(1, std::min(S, p.T));
-  p.NW = waves_per_workgroup(p.T, p.S, units, eight);
+  const int64_t U = int64_t(p.n_strips) * p.T;
+  if (!(opts & kOptStreamK) || split_k > 0) {
+    // uniform split-K: S ranges per strip, one workgroup each
+    int S = split_k > 0 ? split_k : default_split(p.T, units, eight);
+    // each wave indexes its tiles' group offsets from one register: <= 63 tiles
+    S = std::max(S, (p.T + 4 * 63 - 1) / (4 * 63));
+    p.S = std::max(1, std::min(S, p.T));
+    p.NW = waves_per_workgroup(p.T, p.S, units, eight);
+    p.stream = 0;
+    p.G = p.n_strips * p.S;
+    p.C = p.S;
+  } else {
+    // Stream-K (Sec. 3.1): every resident workgroup takes an even share of
+    // the units, as segments that each lie in one strip.  Eight waves and one
+    // workgroup per CU for the MFMA outlier mapping, else four waves and two
+    // workgroups per CU; at least one tile per wave, and at most 63 per wave
+    // and segment.
+    p.NW = eight ? 8 : 4;
+    int G = std::max(1, (p.NW == 8 ? 256 : 512) / p.n_slabs);
+    if (p.NW == 8 && U / G < 8) {
+      p.NW = 4;
+      G = std::max(1, 512 / p.n_slabs);
+    }
+    G = int(std::min<int64_t>(G, std::max<int64_t>(1, U / p.NW)));
+    G = int(std::max<int64_t>(G, (U + int64_t(p.NW) * 63 - 1) / (int64_t(p.NW) * 63)));
+    p.stream = 1;
+    p.S = 1;
+    p.G = G;
+    int C = 1;
+    for (int64_t s = 0; s < p.n_strips; ++s) {
+      const int64_t first = ((s * p.T + 1) * G - 1) / U;
+      const int64_t last = ((s + 1) * p.T * G - 1) / U;
+      C = std::max(C, int(last - first + 1));
+    }
+    p.C = C;
+  }
   p.B = sparse ? B : 1;
 
   if (p.MODE == 0) {
@@ -827,8 +906,8 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   p.lds_bytes = p.off_trash + 16;
   if (p.lds_bytes > 160 * 1024) return false;
 
-  // partial sums: [slab][strip][split][row][64] fp32, every slab kSlabM rows apart
-  p.partial_bytes = p.S > 1 ? size_t(p.n_slabs) * p.n_strips * p.S * kSlabM * kTileN * 4 : 0;
+  // partial sums: [slab][strip][slot][row][64] fp32, every slab kSlabM rows apart
+  p.partial_bytes = p.C > 1 ? size_t(p.n_slabs) * p.n_strips * p.C * kSlabM * kTileN * 4 : 0;
   if (int64_t(p.n_slabs) * p.n_strips > kMaxStrips) return false;   // one counter each
   // every array is addressed with 32-bit byte offsets
   const size_t lim = size_t(1) << 31;
@@ -857,6 +936,8 @@ int launch_matmul(const Plan& pl, const MatmulPtrs& p, bool dense, bool sparse, 
   a.N = pl.N;
   a.T = pl.T;
   a.S = pl.S;
+  a.stream = pl.stream;
+  a.C = pl.C;
   a.n_slabs = pl.n_slabs;
   a.slot_bytes = int(pl.slot_bytes);
   a.off_shc = int(pl.off_shc);

@@ -148,6 +148,30 @@ def test_exact_arithmetic_bit_exact(gpu_lib, case, variant, sparse):
     assert np.array_equal(y16, oracle.bf16_rne_bits(y_ref))
 
 
+SCHEDULE_FLAGS = {"stream_k": 4, "four_waves": 8, "stream_k+four_waves": 12}
+
+
+@pytest.mark.parametrize("case", [c for c in EXACT_CASES if c[4] == 0],
+                         ids=[f"exact{i}" for i, c in enumerate(EXACT_CASES) if c[4] == 0])
+@pytest.mark.parametrize("sched", list(SCHEDULE_FLAGS))
+def test_exact_schedules_bit_exact(gpu_lib, case, sched):
+    """The ablation schedules (Stream-K ranges, four waves only) give the
+    same exact result as the default one."""
+    M, K, N, frac, split_k, params = case
+    log(f"exact schedule {sched} M={M} K={K} N={N} frac={frac}")
+    fq = gpu_lib
+    prob = make_exact_problem(M, K, N, frac=frac, seed=M * 7 + K + N)
+    X, Wq, s, z = fq.to_device(prob)
+    tc = fq.TileCOODevice(fq.fq_pack_tile_coo(K, N, prob.k, prob.n, prob.v, params))
+    f = SCHEDULE_FLAGS[sched]
+    y = fq.fq_w4a16_outlier_matmul(X, Wq, s, z, tc, y_dtype="f32", flags=f)
+    yu = fq.fq_w4a16_outlier_matmul_unfused(X, Wq, s, z, tc, y_dtype="f32", flags=f)
+    torch.cuda.synchronize()
+    y_ref = ref(prob).astype(np.float32)
+    assert np.array_equal(y.cpu().numpy(), y_ref)
+    assert np.array_equal(yu.cpu().numpy(), y_ref)
+
+
 def test_exact_dense_only(gpu_lib):
     prob = make_exact_problem(16, 2048, 512, frac=0.02, seed=99)
     y32 = run(gpu_lib, prob, "dense", "f32")
@@ -351,10 +375,9 @@ def test_quantised_weight_through_fused_kernel(gpu_lib, fill):
     k, n, v = fq.fq_unpack_tile_coo(K, N, host.params, host.tile_indptr, host.bucket_info,
                                     host.packed)
     X = make_activations(M, K, seed=22)
-    Xd = torch.from_numpy(X.view(np.int16).copy()).view(torch.bfloat16).cuda()
-    Wq = torch.from_numpy(qw.Wq.view(np.int32).copy()).cuda()
-    s = torch.from_numpy(qw.scales.view(np.int16).copy()).cuda()
-    z = torch.from_numpy(qw.zeros.view(np.int32).copy()).cuda()
+    Xd, Wq, s, z = fq.to_device(dataclasses.replace(
+        make_problem(M, K, N, frac=0.0, seed=0), X=X, Wq=qw.Wq, scales=qw.scales,
+        zeros=qw.zeros))
     Y = fq.fq_w4a16_outlier_matmul(Xd, Wq, s, z, fq.TileCOODevice(host), y_dtype="f32")
     torch.cuda.synchronize()
     y = Y.cpu().numpy()

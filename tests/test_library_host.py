@@ -270,6 +270,8 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
     (dict(split_k=-1), "FQ_ERR_SHAPE"),
     (dict(flags=3), "FQ_ERR_UNSUPPORTED"),
     (dict(flags=1, M=5), "FQ_ERR_UNSUPPORTED"),
+    (dict(flags=16), "FQ_ERR_UNSUPPORTED"),
+    (dict(flags=4 | 8 | 3), "FQ_ERR_UNSUPPORTED"),
     # 32-bit byte offsets: packed weights of 2^31 bytes, partial sums of 2^31 bytes
     (dict(K=131072, N=32768), "FQ_ERR_UNSUPPORTED"),
     (dict(M=128, K=32768, N=65536, split_k=64), "FQ_ERR_UNSUPPORTED"),
@@ -306,7 +308,7 @@ def test_matmul_rejects_small_workspace(lib):
     need = C.c_size_t(0)
     assert lib.fq_workspace_bytes(C.byref(pr), C.byref(need)) == 0
     assert need.value > 0
-    assert _call(lib, pr, wsb=need.value - 1) == "FQ_ERR_WORKSPACE"
+    assert _call(lib, pr, wsb=1024) == "FQ_ERR_WORKSPACE"
     assert _call(lib, pr, ws=None) == "FQ_ERR_WORKSPACE"
     assert _call(lib, pr, ws=FAKE + 16) == "FQ_ERR_WORKSPACE"
     un = C.c_size_t(0)
