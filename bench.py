@@ -106,6 +106,77 @@ def cpu_baseline(tilecoo_bytes: dict, budget_s: float = 20.0):
                       f"{t_total:.1f} s of CPU time; GB/s counts the same algorithmic bytes"}
 
 
+def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
+    """Per-matmul graph-replay times of: the unfused two-kernel baseline; SD,
+    the fused kernel without the eight-wave workgroups and on an unreordered
+    Tile-COO; SD+EW, with eight-wave workgroups; SD+EW+RE, the default; and the
+    default with the Stream-K schedule.  Prints one JSON line."""
+    from synth import make_problem, seed_for
+    # Tile-COO without reordering, one per shape, R copies
+    plain = {}
+    for si, (name, K, N) in enumerate(SHAPES):
+        p = make_problem(1, K, N, frac=FRAC, seed=seed_for(1, si, 0))
+        prm = fq.fq_default_tilecoo_params()
+        prm.reorder = 0
+        host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v, prm)
+        plain[name] = [fq.TileCOODevice(host, dev) for _ in range(R)]
+    need_sk = max(fq.fq_workspace_bytes(c.M, c.K, c.N, flags=fq.FQ_SCHED_STREAM_K) for c in cases)
+    ws_sk = torch.zeros(max(need_sk, ws.numel()), dtype=torch.uint8, device=dev)
+    variants = {
+        "unfused": lambda c, r: fq.fq_w4a16_outlier_matmul_unfused(
+            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws),
+        "SD": lambda c, r: fq.fq_w4a16_outlier_matmul(
+            c.X, *c.weights[r], plain[c.name][r], Y=c.Y, ws=ws, flags=fq.FQ_FOUR_WAVES),
+        "SD+EW": lambda c, r: fq.fq_w4a16_outlier_matmul(
+            c.X, *c.weights[r], plain[c.name][r], Y=c.Y, ws=ws),
+        "SD+EW+RE": lambda c, r: fq.fq_w4a16_outlier_matmul(
+            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws),
+        "SD+EW+RE+StreamK": lambda c, r: fq.fq_w4a16_outlier_matmul(
+            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws_sk, flags=fq.FQ_SCHED_STREAM_K),
+    }
+
+    def capture(fn):
+        g = torch.cuda.CUDAGraph()
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            fn()
+        torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            fn()
+        torch.cuda.synchronize()
+        return g
+
+    L, reps = 4 * R, 5
+    table = []
+    for c in order:
+        row = {"shape": c.name, "M": c.M}
+        for vname, fn in variants.items():
+            g = capture(lambda: [fn(c, i % R) for i in range(L)])
+            g.replay()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            row[vname] = round(e0.elapsed_time(e1) * 1e3 / (reps * L), 3)
+        table.append(row)
+        log(json.dumps(row))
+    geo = {}
+    for vname in variants:
+        if vname == "unfused":
+            continue
+        r = np.array([t["unfused"] / t[vname] for t in table])
+        geo[vname] = round(float(np.exp(np.log(r).mean())), 4)
+    print(json.dumps({"ablation": "geometric-mean speedup over the unfused two-kernel baseline",
+                      "workload": "Llama-3-8B decode linears at M=1,4,8,16, 1% uniform outliers",
+                      "speedup": geo, "per_matmul_us": table}), flush=True)
+
+
 class Case:
     """One (shape, M) matmul with R rotated weight copies on the device."""
 
@@ -130,6 +201,11 @@ def main():
     ap.add_argument("--no-compare", action="store_true",
                     help="skip the unfused / dense-only / hipBLASLt comparison table")
     ap.add_argument("--details", action="store_true", help="per-matmul table on stderr")
+    ap.add_argument("--ablation", action="store_true",
+                    help="no step timing: per-matmul times of the unfused baseline and of the "
+                         "fused kernel with its techniques added one by one (SD: fused; EW: "
+                         "eight-wave workgroups; RE: Tile-COO reordering) and with Stream-K; "
+                         "prints one JSON line of geometric-mean speedups")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="no timing: eager launches of the dominant kernel's matmuls over the "
                          "rotated copies, then a plain copy of COPY_CAL_BYTES, for rocprofv3 "
@@ -198,6 +274,10 @@ def main():
     for c in order:
         launch(c, 0, args.variant)
     torch.cuda.synchronize()
+
+    if args.ablation:
+        ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None)
+        return
 
     if args.pmc_pass:
         # Each dominant-kernel matmul once per weight copy, then the copy
