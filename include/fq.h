@@ -224,10 +224,11 @@ typedef struct {
  *               bytes, else FQ_ERR_UNSUPPORTED.
  *   group_size  G, must be 128 (one group per 128 x 64 tile).
  *   y_dtype     FQ_Y_BF16 (round to nearest even once, after the full sum) or FQ_Y_F32.
- *   split_k     number of K ranges per 64-column strip; 0 lets the library choose.
+ *   split_k     number of K ranges per output strip; 0 lets the library choose.
  *   flags       bit set: one FQ_SPARSE_* value in bits 0-1 to force the
  *               sparse-path mapping (the library otherwise picks by M), and
- *               the schedule switches FQ_SCHED_STREAM_K and FQ_FOUR_WAVES.
+ *               the schedule switches FQ_SCHED_STREAM_K, FQ_FOUR_WAVES,
+ *               FQ_STRIP_32 and FQ_STRIP_64.
  */
 typedef struct {
   int32_t M;
@@ -255,6 +256,14 @@ enum { FQ_SPARSE_AUTO = 0, FQ_SPARSE_GATHER = 1, FQ_SPARSE_MFMA = 2, FQ_SPARSE_M
  *   FQ_FOUR_WAVES      never run eight waves per workgroup (the extra waves
  *                      that overlap the outlier work with the dense work). */
 enum { FQ_SCHED_STREAM_K = 4, FQ_FOUR_WAVES = 8 };
+
+/* Strip-width switches (fq_problem.flags).  A workgroup computes one output
+ * strip of 32 or 64 columns over its K range.  By default the library uses
+ * 64-column strips when N / 64 strips fill the GPU and 32-column strips
+ * otherwise, so that narrow matrices need no cross-workgroup split-K
+ * reduction.  FQ_STRIP_32 (MFMA outlier mapping only, not with
+ * FQ_SCHED_STREAM_K) and FQ_STRIP_64 force one width. */
+enum { FQ_STRIP_32 = 16, FQ_STRIP_64 = 32 };
 
 /*
  * fq_workspace_bytes -- device workspace the matmul entry points need for

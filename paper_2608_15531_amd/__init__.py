@@ -36,6 +36,8 @@ FQ_SPARSE_MFMA = 2
 _SPARSE_MODES = {"auto": FQ_SPARSE_AUTO, "gather": FQ_SPARSE_GATHER, "mfma": FQ_SPARSE_MFMA}
 FQ_SCHED_STREAM_K = 4
 FQ_FOUR_WAVES = 8
+FQ_STRIP_32 = 16
+FQ_STRIP_64 = 32
 
 
 class FqError(RuntimeError):

@@ -16,8 +16,12 @@ fq_status check_problem(const fq_problem* pr) {
   if (pr->group_size != fqi::kTileK) return FQ_ERR_UNSUPPORTED;
   if (pr->M > fqi::kMaxM) return FQ_ERR_UNSUPPORTED;
   if (pr->y_dtype != FQ_Y_BF16 && pr->y_dtype != FQ_Y_F32) return FQ_ERR_UNSUPPORTED;
-  if (pr->flags & ~(FQ_SPARSE_MASK | FQ_SCHED_STREAM_K | FQ_FOUR_WAVES)) return FQ_ERR_UNSUPPORTED;
+  if (pr->flags & ~(FQ_SPARSE_MASK | FQ_SCHED_STREAM_K | FQ_FOUR_WAVES | FQ_STRIP_32 | FQ_STRIP_64))
+    return FQ_ERR_UNSUPPORTED;
   const int mapping = pr->flags & FQ_SPARSE_MASK;
+  if ((pr->flags & FQ_STRIP_32) &&
+      ((pr->flags & (FQ_STRIP_64 | FQ_SCHED_STREAM_K)) || mapping == FQ_SPARSE_GATHER))
+    return FQ_ERR_UNSUPPORTED;
   if (mapping > FQ_SPARSE_MFMA) return FQ_ERR_UNSUPPORTED;
   if (mapping == FQ_SPARSE_GATHER && pr->M > fqi::kGatherLimitM) return FQ_ERR_UNSUPPORTED;
   return FQ_OK;
@@ -84,7 +88,9 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 int plan_opts(const fq_problem* pr) {
   return ((pr->flags & FQ_SCHED_STREAM_K) ? fqi::kOptStreamK : 0) |
-         ((pr->flags & FQ_FOUR_WAVES) ? fqi::kOptFourWaves : 0);
+         ((pr->flags & FQ_FOUR_WAVES) ? fqi::kOptFourWaves : 0) |
+         ((pr->flags & FQ_STRIP_32) ? fqi::kOptStrip32 : 0) |
+         ((pr->flags & FQ_STRIP_64) ? fqi::kOptStrip64 : 0);
 }
 
 }  // namespace

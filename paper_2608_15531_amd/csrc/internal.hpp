@@ -8,7 +8,7 @@
 namespace fqi {
 
 constexpr int kTileK = 128;     // K side of a dense/sparse tile = quantisation group
-constexpr int kTileN = 64;      // N side of a tile = one output strip
+constexpr int kTileN = 64;      // N side of a Tile-COO tile = widest output strip
 constexpr int kMaxM = 128;      // rows the kernels support
 constexpr int kSlabM = 32;      // rows one workgroup computes (two 16-row MFMA blocks)
 constexpr int kMaxBuckets = 256;
@@ -16,7 +16,7 @@ constexpr int kXStride = 136;   // LDS row stride (elements) of a staged 128-wid
 constexpr int kGatherMaxM = 1;  // up to this M the sparse path gathers X in LDS; above, MFMA
 constexpr int kGatherLimitM = 4; // rows the gather mapping can stage at all
 constexpr int kImageBytes = 16384;   // one wave's B-operand image of a 128 x 64 tile
-// The workspace starts with a fixed counter region (one uint32 per 64-column
+// The workspace starts with a fixed counter region (one uint32 per output
 // strip, zero between calls) so that a workspace shared by problems of
 // different shapes never finds partial sums where a counter is expected.
 constexpr size_t kCounterRegion = 256 * 1024;
@@ -31,7 +31,8 @@ struct Plan {
   int n_slabs;       // 32-row slabs of M, one workgroup set each
   int slab_M;        // rows per slab: min(M, 32)
   int MODE;          // sparse mapping: 0 LDS gathers (M <= kGatherMaxM), 1 MFMA
-  int n_strips;      // N / 64
+  int NCB;           // 16-column MFMA blocks per strip: 2 (32-column strips) or 4 (64)
+  int n_strips;      // N / (16 NCB)
   int T;             // tiles per strip, K / 128
   int S;             // K ranges per strip (explicit split-K); 1 under Stream-K
   int NW;            // waves per workgroup: 4 or 8
@@ -49,6 +50,8 @@ struct Plan {
 // Schedule options of make_plan (bit set).
 constexpr int kOptStreamK = 1;     // Stream-K ranges instead of uniform split-K (split_k == 0)
 constexpr int kOptFourWaves = 2;   // never eight waves per workgroup
+constexpr int kOptStrip32 = 4;     // 32-column strips (MFMA outlier mapping, no Stream-K)
+constexpr int kOptStrip64 = 8;     // 64-column strips
 
 // Returns false when (M, K, N) is outside what the kernels implement.
 // mode: -1 picks the sparse mapping by M, 0 forces gathers, 1 forces MFMA.

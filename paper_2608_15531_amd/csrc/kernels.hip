@@ -56,28 +56,32 @@ namespace fqk {
 constexpr int XS = fqi::kXStride;   // LDS row stride of a staged X slice, elements
 constexpr int kGatherLimitM = fqi::kGatherLimitM;
 
+// Kernel arguments.  The first 64 bytes (one scalar-cache line) hold what
+// every wave needs before its first loads: the schedule and the dense
+// operand pointers.
 struct MatmulArgs {
-  const uint16_t* X;
+  int M, K, N;
+  int T, S;
+  int G;               // workgroups per 32-row slab
+  int n_slabs;         // 32-row slabs of M (grid = workgroups per slab x slabs)
+  int C;               // partial-sum slots per strip (most contributors to one strip)
   const uint32_t* Wq;
   const uint16_t* scales;
   const uint32_t* zeros;
+  const uint16_t* X;
   const uint32_t* tile_indptr;
   const uint4* packed;
-  const float* y_addend;
-  void* Y;
-  float* partials;
-  uint32_t* counters;
   int64_t n_groups;
-  int M, K, N;
   int y_f32;
-  int T, S;
   int stream;          // 1: Stream-K ranges; 0: S uniform splits per strip
-  int C;               // partial-sum slots per strip (most contributors to one strip)
-  int n_slabs;         // 32-row slabs of M (grid = workgroups per slab x slabs)
   int slot_bytes;      // one wave's LDS slot
   int off_shc;         // per-wave sparse output buffers (gather mode)
   int off_flag;
   int off_trash;       // 16 bytes that padding slots are written to (MFMA mode)
+  const float* y_addend;
+  void* Y;
+  float* partials;
+  uint32_t* counters;
 };
 
 // Global loads one tile costs in each mode (each counts once in vmcnt).
@@ -86,21 +90,27 @@ constexpr int loads_per_tile() {
   return (DENSE ? 6 : 0) + (MODE == 0 ? 1 : 4 * MB) + (SPARSE ? 2 : 0);
 }
 
-#ifndef FQ_PIPELINE_DEPTH
-#define FQ_PIPELINE_DEPTH 2
-#endif
-// Tiles in flight per wave.  Two 16-row blocks need twice the activation
-// registers, which leaves room for two buffers only.
-template <int MB>
-constexpr int pipeline_depth() { return MB == 1 ? FQ_PIPELINE_DEPTH : 2; }
+// Tiles in flight per wave.  A 32-column tile takes half the code registers
+// of a 64-column one, which leaves room for four buffers with one 16-row
+// block; two 16-row blocks need twice the activation registers, which
+// leaves room for two buffers only.
+template <int MB, int NCB>
+constexpr int pipeline_depth() { return MB == 1 && NCB == 2 ? 4 : 2; }
+
+// Packed-code words one lane loads per 32-row step: one word per 16-column
+// MFMA block of the strip (NCB blocks: 32-column strips load 8 bytes, 64-column
+// strips 16 bytes), and the fp16 scales of the same columns.
+template <int NCB> struct StripVec;
+template <> struct StripVec<2> { typedef uint2 words; typedef uint32_t scales; };
+template <> struct StripVec<4> { typedef uint4 words; typedef uint2 scales; };
 
 // Everything one wave needs for one tile, held in registers until used.
-template <int MB, int MODE>
+template <int MB, int MODE, int NCB>
 struct TileRegs {
   static constexpr int NX = MODE == 0 ? 1 : 4 * MB;
-  uint4 w[4];      // codes: rows 16t + 4*step + h, columns n0 + 4*c4 .. +3
-  uint2 s;         // fp16 scales of those four columns
-  uint32_t z;      // zero-point word holding those four columns
+  typename StripVec<NCB>::words w[4];   // codes: rows 16t + 4*step + h, columns n0 + NCB*c4 .. + NCB-1
+  typename StripVec<NCB>::scales s;     // fp16 scales of those columns
+  uint32_t z;      // zero-point word holding those columns
   uint4 x[NX];     // MODE 0: X chunk lane (row lane/16, elements 8*(lane%16)..+7)
                    // MODE 1: A fragment [mb][step]: row 16mb + c4, elements 32step + 8h..+7
   uint4 g[2];      // Tile-COO groups lane and lane + 64 of the tile
@@ -132,7 +142,7 @@ __device__ __forceinline__ uint32_t buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t
 template <int MB>
 struct Operands {
   __amdgpu_buffer_rsrc_t w, s, z, x, g;
-  uint32_t lw;       // Wq: row h of a 16-row step block, columns n0 + 4*c4 .. +3
+  uint32_t lw;       // Wq: row h of a 16-row step block, columns n0 + NCB*c4 .. + NCB-1
   uint32_t ls;       // scales of those columns
   uint32_t lz;       // zero-point word holding them
   uint32_t lx[MB];   // X: MODE 0 chunk lane; MODE 1 row 16mb + c4, elements 8h..
@@ -141,16 +151,25 @@ struct Operands {
 // The loads of a tile that do not depend on the Tile-COO offsets: packed
 // codes, scales and zero-points (dense path) and the tile's slice of X.
 // Every load is unconditional (offsets clamped into range) so the compiler
-// counts outstanding loads exactly across the prefetch.
-template <int MB, int MODE, bool DENSE>
+// counts outstanding loads exactly across the prefetch.  A wave-wide load of
+// one step covers 4 packed rows x (16 NCB) columns: 128-byte row segments for
+// 32-column strips, 256-byte ones for 64-column strips.
+template <int MB, int MODE, int NCB, bool DENSE>
 __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Operands<MB>& op,
-                                                int t, int n0, TileRegs<MB, MODE>& r) {
+                                                int t, int n0, TileRegs<MB, MODE, NCB>& r) {
   if (DENSE) {
     const uint32_t step_bytes = uint32_t(a.N) * 16u;   // 4 rows of packed words = 32 k
     const uint32_t wt = (uint32_t(t) * 16u * uint32_t(a.N) + uint32_t(n0)) * 4u;
+    const uint32_t st = (uint32_t(t) * uint32_t(a.N) + uint32_t(n0)) * 2u;
+    if constexpr (NCB == 4) {
 #pragma unroll
-    for (int step = 0; step < 4; ++step) r.w[step] = buf_load16(op.w, op.lw, wt + step * step_bytes);
-    r.s = buf_load8(op.s, op.ls, (uint32_t(t) * uint32_t(a.N) + uint32_t(n0)) * 2u);
+      for (int step = 0; step < 4; ++step) r.w[step] = buf_load16(op.w, op.lw, wt + step * step_bytes);
+      r.s = buf_load8(op.s, op.ls, st);
+    } else {
+#pragma unroll
+      for (int step = 0; step < 4; ++step) r.w[step] = buf_load8(op.w, op.lw, wt + step * step_bytes);
+      r.s = buf_load4(op.s, op.ls, st);
+    }
     r.z = buf_load4(op.z, op.lz, (uint32_t(t) * uint32_t(a.N >> 3) + uint32_t(n0 >> 3)) * 4u);
   }
   const uint32_t xt = uint32_t(t) * 256u;
@@ -165,9 +184,9 @@ __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Opera
 }
 
 // The tile's first two Tile-COO groups, one per lane and half-wave pass.
-template <int MB, int MODE, bool SPARSE>
+template <int MB, int MODE, int NCB, bool SPARSE>
 __device__ __forceinline__ void load_tile_sparse(const Operands<MB>& op, int lane, uint32_t g0,
-                                                 uint32_t g1, TileRegs<MB, MODE>& r) {
+                                                 uint32_t g1, TileRegs<MB, MODE, NCB>& r) {
   if (SPARSE) {
     r.g0 = g0;
     r.g1 = g1;
@@ -270,23 +289,36 @@ __device__ __forceinline__ void sparse_gather(const MatmulArgs& a, const uint16_
   }
 }
 
-// MFMA mode: the B-operand image of a tile.  Element (k, n) of the tile is
-// read by lane (n/4 + 16 * ((k%32)/8)) as B of MFMA (step k/32, column block
-// n%4), at the position its X partner holds k (chunk order x0,x4,x1,x5,...).
-// As a bf16 index into the wave's 16 KB image its bits are
-//   0: k2 | 1-2: k0,k1 | 3-6: n2..n5 | 7-8: k3,k4 | 9-10: n0,n1 | 11-12: k5,k6.
+// MFMA mode: the B-operand image of a strip's tile (128 rows x 16 NCB
+// columns).  Local column n' of the strip belongs to MFMA column block
+// j = n' % NCB at position c = n' / NCB, so element (k, n') is read by lane
+// (c + 16 * ((k%32)/8)) as B of MFMA (step k/32, block j), at the position its
+// X partner holds k (chunk order x0,x4,x1,x5,...).  As a bf16 index into the
+// wave's image its bits are, for 64-column strips (NCB = 4, 16 KB image)
+//   0: k2 | 1-2: k0,k1 | 3-6: n'2..n'5 | 7-8: k3,k4 | 9-10: n'0,n'1 | 11-12: k5,k6
+// and for 32-column strips (NCB = 2, 8 KB image)
+//   0: k2 | 1-2: k0,k1 | 3-6: n'1..n'4 | 7-8: k3,k4 | 9: n'0 | 10-11: k5,k6.
 // image_offsets forms the four byte offsets of a group at once, one slot per
 // byte lane while the index is split into its low and high bytes, then two
-// slots per dword (16-bit halves; the offsets are below 2^14).
+// slots per dword (16-bit halves; the offsets are below 2^14).  C holds the
+// Tile-COO columns (0..63); a 32-column strip uses their low five bits.
+template <int NCB>
 __device__ __forceinline__ void image_offsets(uint32_t R, uint32_t C, uint32_t& o01, uint32_t& o23) {
-  const uint32_t r1 = R << 1, r2 = R >> 2, c1 = C << 1;
+  const uint32_t r1 = R << 1, r2 = R >> 2;
   uint32_t lo = r2 & 0x01010101u;               // k2
   lo = and_or(r1, 0x06060606u, lo);             // k0, k1
-  lo = and_or(c1, 0x78787878u, lo);             // n2..n5
-  lo = and_or(R << 4, 0x80808080u, lo);         // k3
   uint32_t hi = (R >> 4) & 0x01010101u;         // k4
-  hi = and_or(c1, 0x06060606u, hi);             // n0, n1
-  hi = and_or(r2, 0x18181818u, hi);             // k5, k6
+  if constexpr (NCB == 4) {
+    const uint32_t c1 = C << 1;
+    lo = and_or(c1, 0x78787878u, lo);           // n'2..n'5
+    hi = and_or(c1, 0x06060606u, hi);           // n'0, n'1
+    hi = and_or(r2, 0x18181818u, hi);           // k5, k6
+  } else {
+    lo = and_or(C << 2, 0x78787878u, lo);       // n'1..n'4
+    hi = and_or(C << 1, 0x02020202u, hi);       // n'0
+    hi = and_or(R >> 3, 0x0C0C0C0Cu, hi);       // k5, k6
+  }
+  lo = and_or(R << 4, 0x80808080u, lo);         // k3
   // [lo0 hi0 lo1 hi1] and [lo2 hi2 lo3 hi3], then element -> byte offset
   o01 = __builtin_amdgcn_perm(hi, lo, 0x05010400u) << 1;
   o23 = __builtin_amdgcn_perm(hi, lo, 0x07030602u) << 1;
@@ -306,17 +338,22 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
 }
 
 // Writes a group's four values into the image at absolute LDS address `img`
-// and returns where they went: a padding slot (value bits 0) goes to the
+// and returns where they went.  A padding slot (value bits 0) goes to the
 // trash word instead, since its position may coincide with a real element of
-// another group.
+// another group, and so does a slot whose column lies in the other half of a
+// 64-column Tile-COO tile when the strip is 32 columns wide (`half` = which
+// half this strip is; bit 5 of a column selects the half).
+template <int NCB>
 __device__ __forceinline__ void scatter_group(uint32_t img, uint32_t trash, uint4 raw,
-                                              uint32_t addr[4]) {
+                                              uint32_t half, uint32_t addr[4]) {
   uint32_t o01, o23;
-  image_offsets(raw.x, raw.y, o01, o23);
-  addr[0] = (raw.z & 0xFFFFu) != 0u ? img + (o01 & 0xFFFFu) : trash;
-  addr[1] = raw.z > 0xFFFFu ? img + (o01 >> 16) : trash;
-  addr[2] = (raw.w & 0xFFFFu) != 0u ? img + (o23 & 0xFFFFu) : trash;
-  addr[3] = raw.w > 0xFFFFu ? img + (o23 >> 16) : trash;
+  image_offsets<NCB>(raw.x, raw.y, o01, o23);
+  // per slot: bit 5 of its column equals `half` (always true for NCB = 4)
+  const uint32_t other = NCB == 4 ? 0u : ((raw.y >> 5) ^ (half * 0x01010101u)) & 0x01010101u;
+  addr[0] = (raw.z & 0xFFFFu) != 0u && !(other & 0x1u) ? img + (o01 & 0xFFFFu) : trash;
+  addr[1] = raw.z > 0xFFFFu && !(other & 0x100u) ? img + (o01 >> 16) : trash;
+  addr[2] = (raw.w & 0xFFFFu) != 0u && !(other & 0x10000u) ? img + (o23 & 0xFFFFu) : trash;
+  addr[3] = raw.w > 0xFFFFu && !(other & 0x1000000u) ? img + (o23 >> 16) : trash;
   lds_store16(addr[0], raw.z);
   lds_store16(addr[1], raw.z >> 16);
   lds_store16(addr[2], raw.w);
@@ -328,8 +365,10 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
   for (int j = 0; j < 4; ++j) lds_store16(addr[j], 0u);
 }
 
-template <int MB, int MODE, bool DENSE, bool SPARSE, int NW, bool SK>
+template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK>
 __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
+  static_assert(NCB == 4 || (NCB == 2 && MODE == 1), "32-column strips use the MFMA outlier mapping");
+  constexpr int NC = 16 * NCB;                 // strip width, columns
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -347,10 +386,15 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   // give each XCD a contiguous run of workgroups so that neighbouring ranges
   // share an L2, and deal the row slabs of one range to the same XCD one after
   // another, so that all but the first read its weights from that L2.
-  const int G = gridDim.x / args.n_slabs;   // workgroups per slab
+  // All of this is wave-uniform scalar arithmetic on 32-bit values: it runs
+  // before the first load of every wave, so it is kept short.
+  const int G = args.G;                     // workgroups per slab
   const int bid = blockIdx.x;
   int wg, slab;
-  if ((G & 7) == 0) {
+  if (args.n_slabs == 1) {
+    slab = 0;
+    wg = (G & 7) == 0 ? (bid & 7) * (G >> 3) + (bid >> 3) : bid;
+  } else if ((G & 7) == 0) {
     const int t = bid >> 3;
     slab = t % args.n_slabs;
     wg = (bid & 7) * (G >> 3) + t / args.n_slabs;
@@ -361,28 +405,33 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   // This workgroup's rows [m0, m0 + M) as a problem of its own.
   MatmulArgs a = args;
   const int m0 = slab * fqi::kSlabM;
-  const int n_strips = args.N / 64;
+  const int n_strips = args.N / NC;
   a.M = min(fqi::kSlabM, args.M - m0);
   a.X = args.X + size_t(m0) * args.K;
   a.Y = static_cast<char*>(args.Y) + size_t(m0) * args.N * (args.y_f32 ? 4 : 2);
   if (args.y_addend) a.y_addend = args.y_addend + size_t(m0) * args.N;
-  a.partials = args.partials + size_t(slab) * n_strips * args.C * fqi::kSlabM * 64;
+  a.partials = args.partials + size_t(slab) * n_strips * args.C * fqi::kSlabM * NC;
   a.counters = args.counters + size_t(slab) * n_strips;
-  const int64_t U = int64_t(n_strips) * a.T;
-  int64_t u_begin, u_end;
+  // Uniform split-K: workgroup wg is K range sp of strip st (32-bit math;
+  // no division at all without a split).  Stream-K: an even share of the
+  // U = strips x tiles units, as 64-bit ranges.
+  int st = wg, sp = 0;
+  if (!SK && a.S > 1) {
+    st = wg / a.S;
+    sp = wg - st * a.S;
+  }
+  const int64_t U = SK ? int64_t(n_strips) * a.T : 0;
+  int64_t u_begin = 0, u_end = 0;
   if (SK) {
     u_begin = int64_t(wg) * U / G;
     u_end = int64_t(wg + 1) * U / G;
-  } else {
-    const int st = wg / a.S, sp = wg - st * a.S;
-    u_begin = int64_t(st) * a.T + int64_t(sp) * a.T / a.S;
-    u_end = int64_t(st) * a.T + int64_t(sp + 1) * a.T / a.S;
   }
 
   unsigned char* slot = smem + size_t(wave) * a.slot_bytes;
   uint16_t* xs = reinterpret_cast<uint16_t*>(slot);   // MODE 0: X slice
   uint16_t* bo = reinterpret_cast<uint16_t*>(slot);   // MODE 1: B-operand image
   static_assert(MODE != 1 || !SPARSE || fqi::kImageBytes == 16384, "image layout");
+  constexpr int kImageBlocks = 4 * NCB;        // 1 KB MFMA B-operand blocks per image
   // Each wave owns its sparse output buffer (gather mode): within a wave the
   // LDS unit applies adds in a fixed order, so repeated calls are identical.
   float* shc_all = reinterpret_cast<float*>(smem + a.off_shc);
@@ -399,9 +448,9 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   op.z = make_rsrc(a.zeros, uint32_t(a.K / 128) * uint32_t(a.N / 8) * 4u);
   op.x = make_rsrc(a.X, uint32_t(a.M) * uint32_t(a.K) * 2u);
   op.g = make_rsrc(a.packed, uint32_t(max(a.n_groups, int64_t(1))) * 16u);
-  op.lw = uint32_t(h * a.N + 4 * c4) * 4u;
-  op.ls = uint32_t(c4) * 8u;
-  op.lz = uint32_t(c4 >> 1) * 4u;
+  op.lw = uint32_t(h * a.N + NCB * c4) * 4u;
+  op.ls = uint32_t(c4) * (2u * NCB);
+  op.lz = uint32_t((NCB * c4) >> 3) * 4u;
   if (MODE == 0) {
     // rows past M load row M-1 (the slice store below is then a rewrite)
     op.lx[0] = (uint32_t(min(lane >> 4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(lane & 15)) * 2u;
@@ -416,25 +465,26 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
 
   // The current segment (read by the lambdas below).
   int strip = 0, n0 = 0, w_lo = 0, w_hi = 0;
+  uint32_t half = 0;   // 32-column strips: which half of the 64-column Tile-COO tile
   int64_t tile_base = 0;
   uint32_t tp = 0;
-  f32x4_t acc[MB][4];
+  f32x4_t acc[MB][NCB];
 
-  auto issue_sparse = [&](int t, TileRegs<MB, MODE>& r) __attribute__((always_inline)) {
+  auto issue_sparse = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
     uint32_t g0 = 0, g1 = 0;
     if (SPARSE) {
       const uint32_t ng = uint32_t(a.n_groups);   // < 2^27, checked on the host
       g0 = min(uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo)), ng);
       g1 = max(g0, min(uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo + 1)), ng));
     }
-    load_tile_sparse<MB, MODE, SPARSE>(op, lane, g0, g1, r);
+    load_tile_sparse<MB, MODE, NCB, SPARSE>(op, lane, g0, g1, r);
   };
-  auto issue = [&](int t, TileRegs<MB, MODE>& r) __attribute__((always_inline)) {
-    load_tile_dense<MB, MODE, DENSE>(a, op, t, n0, r);
+  auto issue = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
+    load_tile_dense<MB, MODE, NCB, DENSE>(a, op, t, n0, r);
     issue_sparse(t, r);
   };
 
-  auto compute = [&](const TileRegs<MB, MODE>& cur) __attribute__((always_inline)) {
+  auto compute = [&](const TileRegs<MB, MODE, NCB>& cur) __attribute__((always_inline)) {
     // ---- X fragments
     bf16x8_t A[MB][4];
     if (MODE == 0) {
@@ -455,56 +505,29 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
           A[mb][step] = __builtin_bit_cast(bf16x8_t, permute_chunk(cur.x[mb * 4 + step]));
     }
 
-    // ---- scatter the tile's outliers (MFMA mode); overlaps the dense MFMAs
-    uint32_t n_g = 0;
-    if (SPARSE) n_g = cur.g1 - cur.g0;
-    uint32_t addr[2][4];
-    if (SPARSE && MODE == 1) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        if (uint32_t(lane + 64 * j) < n_g) scatter_group(img, trash, cur.g[j], addr[j]);
-      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
-        uint32_t ad[4];
-        scatter_group(img, trash, a.packed[cur.g0 + gi], ad);
-      }
-      __builtin_amdgcn_wave_barrier();
-    }
-
-    // ---- gather mapping: the first two groups' X values, read before the
-    // dense work so their LDS latency is hidden
-    Gathered gx[2];
-    bool gsingle[2] = {false, false};
-    if (SPARSE && MODE == 0) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        gsingle[j] = uint32_t(lane + 64 * j) < n_g && single_column(decode_group(cur.g[j]));
-        if (gsingle[j]) gather_x(a, xs, cur.g[j], gx[j]);
-      }
-    }
-
-    // ---- dense path, with the MFMA mapping's outlier MFMAs interleaved per
-    // 32-row step: the step's four image blocks are read from LDS before its
-    // dequantisation and multiplied after it
+    // ---- dense path: per 32-row step, dequantise the lane's words and
+    // multiply; one more MFMA against ones gives the rows' sums of X.  It
+    // comes first so that a tile's dense work never waits for its Tile-COO
+    // groups, whose loads depend on tile_indptr and are issued last.
     constexpr bool SPM = SPARSE && MODE == 1;
-    const uint4* b4 = reinterpret_cast<const uint4*>(bo);
-    f32x4_t tmp[MB][4], xsum[MB];
+    f32x4_t tmp[MB][NCB], xsum[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       xsum[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < 4; ++c) tmp[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int c = 0; c < NCB; ++c) tmp[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
+    if (DENSE) {
 #pragma unroll
-    for (int step = 0; step < 4; ++step) {
-      bf16x8_t Bo[4];
-      if (SPM) {
+      for (int step = 0; step < 4; ++step) {
+        uint32_t w4[NCB];
+        if constexpr (NCB == 4) {
+          w4[0] = cur.w[step].x; w4[1] = cur.w[step].y; w4[2] = cur.w[step].z; w4[3] = cur.w[step].w;
+        } else {
+          w4[0] = cur.w[step].x; w4[1] = cur.w[step].y;
+        }
 #pragma unroll
-        for (int c = 0; c < 4; ++c) Bo[c] = __builtin_bit_cast(bf16x8_t, b4[(step * 4 + c) * 64 + lane]);
-      }
-      if (DENSE) {
-        const uint32_t w4[4] = {cur.w[step].x, cur.w[step].y, cur.w[step].z, cur.w[step].w};
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
+        for (int c = 0; c < NCB; ++c) {
           const bf16x8_t Bq = dequant_word(w4[c]);
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
@@ -514,30 +537,73 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
         for (int mb = 0; mb < MB; ++mb)
           xsum[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], ones, xsum[mb], 0, 0, 0);
       }
-      if (SPM) {
+    }
+
+    // ---- dense epilogue: eq. (3) once per (group, column) in fp32.  Rows
+    // 4h + r with r >= M (M < 4) never reach the output: skip them.
+    if (DENSE) {
+      float sc[NCB], zf[NCB];
+      if constexpr (NCB == 4) {
+        sc[0] = f16_bits_to_f32(cur.s.x & 0xFFFFu);
+        sc[1] = f16_bits_to_f32(cur.s.x >> 16);
+        sc[2] = f16_bits_to_f32(cur.s.y & 0xFFFFu);
+        sc[3] = f16_bits_to_f32(cur.s.y >> 16);
+      } else {
+        sc[0] = f16_bits_to_f32(cur.s & 0xFFFFu);
+        sc[1] = f16_bits_to_f32(cur.s >> 16);
+      }
+      // the lane's columns n0 + NCB*c4 + c sit at nibbles (NCB*c4) % 8 + c of the word
+      const int zsh = ((NCB * c4) & 7) * 4;
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+      for (int c = 0; c < NCB; ++c) zf[c] = kCodeOffset + float((cur.z >> (zsh + 4 * c)) & 15u);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (MB == 1 && r > 0 && r >= a.M) break;
+#pragma unroll
+          for (int c = 0; c < NCB; ++c)
+            acc[mb][c][r] += sc[c] * (tmp[mb][c][r] - zf[c] * xsum[mb][r]);
+        }
+    }
+
+    // ---- sparse path, MFMA mapping: scatter the tile's outliers into the
+    // image, read it back per step and multiply into the output tile
+    uint32_t n_g = 0;
+    if (SPARSE) n_g = cur.g1 - cur.g0;
+    uint32_t addr[2][4];
+    if (SPM) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        if (uint32_t(lane + 64 * j) < n_g) scatter_group<NCB>(img, trash, cur.g[j], half, addr[j]);
+      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
+        uint32_t ad[4];
+        scatter_group<NCB>(img, trash, a.packed[cur.g0 + gi], half, ad);
+      }
+      __builtin_amdgcn_wave_barrier();
+      const uint4* b4 = reinterpret_cast<const uint4*>(bo);
+#pragma unroll
+      for (int step = 0; step < 4; ++step) {
+        bf16x8_t Bo[NCB];
+#pragma unroll
+        for (int c = 0; c < NCB; ++c) Bo[c] = __builtin_bit_cast(bf16x8_t, b4[(step * NCB + c) * 64 + lane]);
+#pragma unroll
+        for (int c = 0; c < NCB; ++c)
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
             acc[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bo[c], acc[mb][c], 0, 0, 0);
       }
     }
-    if (DENSE) {
-      float sc[4], zf[4];
-      sc[0] = f16_bits_to_f32(cur.s.x & 0xFFFFu);
-      sc[1] = f16_bits_to_f32(cur.s.x >> 16);
-      sc[2] = f16_bits_to_f32(cur.s.y & 0xFFFFu);
-      sc[3] = f16_bits_to_f32(cur.s.y >> 16);
-      const int zsh = (c4 & 1) * 16;
+
+    // ---- gather mapping: the first two groups' X values from the staged slice
+    Gathered gx[2];
+    bool gsingle[2] = {false, false};
+    if (SPARSE && MODE == 0) {
 #pragma unroll
-      for (int c = 0; c < 4; ++c) zf[c] = kCodeOffset + float((cur.z >> (zsh + 4 * c)) & 15u);
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            acc[mb][c][r] += sc[c] * (tmp[mb][c][r] - zf[c] * xsum[mb][r]);
+      for (int j = 0; j < 2; ++j) {
+        gsingle[j] = uint32_t(lane + 64 * j) < n_g && single_column(decode_group(cur.g[j]));
+        if (gsingle[j]) gather_x(a, xs, cur.g[j], gx[j]);
+      }
     }
 
     // ---- MFMA mapping: restore the zeros of the image
@@ -549,7 +615,7 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
       for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
         uint32_t o01, o23;
         const uint4 raw = a.packed[cur.g0 + gi];
-        image_offsets(raw.x, raw.y, o01, o23);
+        image_offsets<NCB>(raw.x, raw.y, o01, o23);
         const uint32_t ad[4] = {img + (o01 & 0xFFFFu), img + (o01 >> 16), img + (o23 & 0xFFFFu),
                                 img + (o23 >> 16)};
         clear_group(ad);   // zeros everywhere the group could have written
@@ -573,37 +639,53 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   // accesses, the encoding of relaxed agent-scope atomics; no cache-wide
   // writeback or invalidate is issued.
   const __amdgpu_buffer_rsrc_t prs =
-      make_rsrc(a.partials, uint32_t(n_strips) * uint32_t(a.C) * uint32_t(a.M) * 256u);
+      make_rsrc(a.partials, uint32_t(n_strips) * uint32_t(a.C) * uint32_t(a.M) * (4u * NC));
 
-  for (int64_t u = u_begin; u < u_end;) {
+  for (int64_t u = u_begin;;) {
     // ------------------------------------------------------------ segment
-    strip = int(u / a.T);
-    const int t_lo = int(u - int64_t(strip) * a.T);
-    const int t_hi = int(min(int64_t(a.T), int64_t(t_lo) + (u_end - u)));
-    u += t_hi - t_lo;
-    // contributors to this strip, and this workgroup's place among them
-    int n_contrib, my_slot;
-    if (SK) {
+    // this workgroup's tiles [t_lo, t_hi) of the strip, the number of
+    // workgroups contributing to the strip and this one's place among them
+    int t_lo, t_hi, n_contrib, my_slot;
+    if constexpr (SK) {
+      if (u >= u_end) break;
+      strip = int(u / a.T);
+      t_lo = int(u - int64_t(strip) * a.T);
+      t_hi = int(min(int64_t(a.T), int64_t(t_lo) + (u_end - u)));
+      u += t_hi - t_lo;
       const int64_t first = ((int64_t(strip) * a.T + 1) * G - 1) / U;
       const int64_t last = (int64_t(strip + 1) * a.T * G - 1) / U;
       n_contrib = int(last - first + 1);
       my_slot = int(wg - first);
     } else {
+      strip = st;
       n_contrib = a.S;
-      my_slot = wg - (wg / a.S) * a.S;
+      my_slot = sp;
+      if (a.S == 1) {
+        t_lo = 0;
+        t_hi = a.T;
+      } else {
+        t_lo = int(uint32_t(sp * a.T) / uint32_t(a.S));
+        t_hi = int(uint32_t((sp + 1) * a.T) / uint32_t(a.S));
+      }
     }
-    const int nt = t_hi - t_lo;
-    w_lo = t_lo + (nt * wave) / NW;    // this wave's tiles [w_lo, w_hi)
-    w_hi = t_lo + (nt * (wave + 1)) / NW;
-    n0 = strip * 64;
-    tile_base = int64_t(strip) * a.T;
+    strip = __builtin_amdgcn_readfirstlane(strip);
+    t_lo = __builtin_amdgcn_readfirstlane(t_lo);
+    t_hi = __builtin_amdgcn_readfirstlane(t_hi);
+    const uint32_t nt = uint32_t(t_hi - t_lo);
+    w_lo = t_lo + int(nt * uint32_t(wave) / NW);    // this wave's tiles [w_lo, w_hi)
+    w_hi = t_lo + int(nt * uint32_t(wave + 1) / NW);
+    n0 = strip * NC;
+    // Tile-COO tiles are 128 x 64 and stored strip-major: a 32-column strip
+    // reads the tiles of its 64-column strip and keeps its half's columns
+    tile_base = int64_t(uint32_t(NCB == 4 ? strip : strip >> 1) * uint32_t(a.T));
+    half = NCB == 4 ? 0u : uint32_t(strip & 1);
 
     if (SPARSE && MODE == 0)
       for (int i = lane; i < a.M * 64; i += 64) shc[i] = 0.f;
     if (SPARSE && MODE == 1) {
       uint4* b4 = reinterpret_cast<uint4*>(bo);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) b4[i * 64 + lane] = uint4{0u, 0u, 0u, 0u};
+      for (int i = 0; i < kImageBlocks; ++i) b4[i * 64 + lane] = uint4{0u, 0u, 0u, 0u};
     }
     // Group offsets of this wave's tiles: lane i holds tile_indptr[w_lo + i].
     // The value is used raw (clamped only when read) so that nothing waits
@@ -614,7 +696,7 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int c = 0; c < 4; ++c) acc[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int c = 0; c < NCB; ++c) acc[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     // D register buffers, all in flight: while tile t is computed from one,
     // the loads of tiles t+1 .. t+D-1 fill the others; when t is done its
@@ -626,15 +708,15 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
     // on every entry; sched_barrier keeps the scheduler from sinking a tile's
     // loads below the next wait, which would cut the prefetch depth.
     constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
-    constexpr int D = pipeline_depth<MB>();
-    TileRegs<MB, MODE> rg[D];
+    constexpr int D = pipeline_depth<MB, NCB>();
+    TileRegs<MB, MODE, NCB> rg[D];
     if (w_lo < w_hi) {
       const int last = w_hi - 1;
       // The first tiles' dense loads go out before the group offsets have
       // arrived; only the group loads wait for them.
   #pragma unroll
       for (int i = 0; i < D; ++i) {
-        load_tile_dense<MB, MODE, DENSE>(a, op, min(w_lo + i, last), n0, rg[i]);
+        load_tile_dense<MB, MODE, NCB, DENSE>(a, op, min(w_lo + i, last), n0, rg[i]);
         __builtin_amdgcn_sched_barrier(0);
       }
   #pragma unroll
@@ -676,28 +758,35 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = mb * 16 + 4 * h + r;
-        if (row < a.M)
-          *reinterpret_cast<f32x4_t*>(red + (wave * a.M + row) * 64 + 4 * c4) =
-              f32x4_t{acc[mb][0][r], acc[mb][1][r], acc[mb][2][r], acc[mb][3][r]};
+        if (row < a.M) {
+          float* dst = red + (wave * a.M + row) * NC + NCB * c4;
+          if constexpr (NCB == 4)
+            *reinterpret_cast<f32x4_t*>(dst) = f32x4_t{acc[mb][0][r], acc[mb][1][r], acc[mb][2][r], acc[mb][3][r]};
+          else
+            *reinterpret_cast<float2*>(dst) = float2{acc[mb][0][r], acc[mb][1][r]};
+        }
       }
     __syncthreads();
 
+    // 16-byte column quads of the strip: NC / 4 per row
+    constexpr int QPR = NC / 4;
     const bool shared = n_contrib > 1;
-    const uint32_t strip_part = uint32_t(strip) * uint32_t(a.C) * uint32_t(a.M) * 256u;  // bytes
-    for (int i = tid; i < a.M * 16; i += 64 * NW) {
-      const int m = i >> 4;
-      const int cq = i & 15;
+    const uint32_t row_bytes = 4u * NC;
+    const uint32_t strip_part = uint32_t(strip) * uint32_t(a.C) * uint32_t(a.M) * row_bytes;
+    for (int i = tid; i < a.M * QPR; i += 64 * NW) {
+      const int m = i / QPR;
+      const int cq = i - m * QPR;
       f32x4_t v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int w = 0; w < NW; ++w)
-        v += *reinterpret_cast<const f32x4_t*>(red + (w * a.M + m) * 64 + 4 * cq);
+        v += *reinterpret_cast<const f32x4_t*>(red + (w * a.M + m) * NC + 4 * cq);
       if (SPARSE && MODE == 0) {
 #pragma unroll
         for (int w = 0; w < NW; ++w)
           v += *reinterpret_cast<const f32x4_t*>(shc_all + (w * a.M + m) * 64 + 4 * cq);
       }
       if (shared) {
-        const uint32_t off = strip_part + uint32_t(my_slot * a.M + m) * 256u + uint32_t(cq) * 16u;
+        const uint32_t off = strip_part + uint32_t(my_slot * a.M + m) * row_bytes + uint32_t(cq) * 16u;
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), prs, int(off), 0, kSc1);
       } else {
         store_out(a, m, n0 + 4 * cq, v);
@@ -716,11 +805,11 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
         // The last contributor adds the partials in contributor order, with
         // up to eight loads in flight per thread.
         constexpr int kBatch = 8;
-        for (int i = tid; i < a.M * 16; i += 64 * NW) {
-          const int m = i >> 4;
-          const int cq = i & 15;
-          const uint32_t base = strip_part + uint32_t(m) * 256u + uint32_t(cq) * 16u;
-          const uint32_t slot_stride = uint32_t(a.M) * 256u;
+        for (int i = tid; i < a.M * QPR; i += 64 * NW) {
+          const int m = i / QPR;
+          const int cq = i - m * QPR;
+          const uint32_t base = strip_part + uint32_t(m) * row_bytes + uint32_t(cq) * 16u;
+          const uint32_t slot_stride = uint32_t(a.M) * row_bytes;
           f32x4_t v{0.f, 0.f, 0.f, 0.f};
           for (int s0 = 0; s0 < n_contrib; s0 += kBatch) {
             u32x4_t part[kBatch];
@@ -770,9 +859,9 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
   }
 }
 
-template <int MB, int MODE, bool DENSE, bool SPARSE, int NW, bool SK>
+template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, MODE, DENSE, SPARSE, NW, SK>;
+  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK>;
   if (pl.lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -784,23 +873,35 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
   return int(hipGetLastError());
 }
 
-template <int MB, int MODE, int NW, bool SK>
+template <int MB, int MODE, int NCB, int NW, bool SK>
 int launch_sched(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
-  if (dense && sparse) return launch_variant<MB, MODE, true, true, NW, SK>(pl, a, s);
-  if (dense) return launch_variant<MB, MODE, true, false, NW, SK>(pl, a, s);
-  return launch_variant<MB, MODE, false, true, NW, SK>(pl, a, s);
+  if (dense && sparse) return launch_variant<MB, MODE, NCB, true, true, NW, SK>(pl, a, s);
+  if (dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK>(pl, a, s);
+  return launch_variant<MB, MODE, NCB, false, true, NW, SK>(pl, a, s);
 }
 
-template <int MB, int MODE, int NW>
+// Stream-K is built for 64-column strips only (the plan never combines it
+// with 32-column strips).
+template <int MB, int MODE, int NCB, int NW>
 int launch_waves(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
-  return pl.stream ? launch_sched<MB, MODE, NW, true>(pl, a, dense, sparse, s)
-                   : launch_sched<MB, MODE, NW, false>(pl, a, dense, sparse, s);
+  if constexpr (NCB == 4) {
+    if (pl.stream) return launch_sched<MB, MODE, NCB, NW, true>(pl, a, dense, sparse, s);
+  }
+  return launch_sched<MB, MODE, NCB, NW, false>(pl, a, dense, sparse, s);
+}
+
+template <int MB, int MODE, int NCB>
+int launch_strip(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
+  return pl.NW == 8 ? launch_waves<MB, MODE, NCB, 8>(pl, a, dense, sparse, s)
+                    : launch_waves<MB, MODE, NCB, 4>(pl, a, dense, sparse, s);
 }
 
 template <int MB, int MODE>
 int launch_mode(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
-  return pl.NW == 8 ? launch_waves<MB, MODE, 8>(pl, a, dense, sparse, s)
-                    : launch_waves<MB, MODE, 4>(pl, a, dense, sparse, s);
+  if constexpr (MODE == 1) {
+    if (pl.NCB == 2) return launch_strip<MB, MODE, 2>(pl, a, dense, sparse, s);
+  }
+  return launch_strip<MB, MODE, 4>(pl, a, dense, sparse, s);
 }
 
 }  // namespace fqk
@@ -810,15 +911,15 @@ namespace fqi {
 namespace {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Grid shape under split-K.  The fused kernel with the MFMA outlier mapping
-// is bound by per-SIMD issue (dequantisation VALU, MFMA and the LDS image of
-// the outliers), so when the strips fit the CUs it runs eight waves per
-// workgroup -- two per SIMD, overlapping one another's VALU, MFMA and LDS
-// work -- with the largest split that keeps at most one workgroup per CU
-// and one tile per wave.  Otherwise (dense only, the gather mapping, or more
-// strips than CUs) four waves per workgroup and the smallest split that
-// reaches about one workgroup per CU, at least one tile per wave; wide
-// matrices need no split.
+// Grid shape with 64-column strips under split-K.  The fused kernel with the
+// MFMA outlier mapping is bound by per-SIMD issue (dequantisation VALU, MFMA
+// and the LDS image of the outliers), so when the strips fit the CUs it runs
+// eight waves per workgroup -- two per SIMD, overlapping one another's VALU,
+// MFMA and LDS work -- with the largest split that keeps at most one
+// workgroup per CU and one tile per wave.  Otherwise (dense only, the gather
+// mapping, or more strips than CUs) four waves per workgroup and the smallest
+// split that reaches about one workgroup per CU, at least one tile per wave;
+// wide matrices need no split.
 int default_split(int T, int n_strips, bool eight_waves) {
   int S = 1;
   if (eight_waves && n_strips <= 256) {
@@ -832,6 +933,19 @@ int default_split(int T, int n_strips, bool eight_waves) {
 int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
   return (eight_waves && int64_t(n_strips) * S <= 256 && T / S >= 8) ? 8 : 4;
 }
+
+// Strip width.  32-column strips (128-byte segments of each packed row,
+// which stream as well as 256-byte ones) let a narrow matrix cover the GPU
+// without a cross-workgroup split, but cost about 1.5x the instructions per
+// byte (the activation permute, the per-tile epilogue and the outlier pass
+// are shared by half as many columns) and measured slower than 64-column
+// strips with split-K on every Llama-3 decode shape, so 64 is the default.
+int choose_ncb(int N, int n_slabs, int mode, int opts) {
+  (void)N;
+  (void)n_slabs;
+  (void)mode;
+  return (opts & kOptStrip32) ? 2 : 4;
+}
 }  // namespace
 
 bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
@@ -840,6 +954,7 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   if (M < 1 || M > kMaxM || K < kTileK || N < kTileN || K % kTileK || N % kTileN) return false;
   if (N / kTileN > kMaxStrips) return false;
   if (sparse && (B < 1 || B > kMaxBuckets)) return false;
+  if ((opts & kOptStrip32) && (opts & (kOptStrip64 | kOptStreamK))) return false;
   Plan p{};
   p.M = M;
   p.K = K;
@@ -847,16 +962,31 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   p.n_slabs = (M + kSlabM - 1) / kSlabM;
   p.slab_M = std::min(M, kSlabM);
   p.MB = p.slab_M <= 16 ? 1 : 2;
-  p.MODE = mode >= 0 ? mode : (M <= kGatherMaxM ? 0 : 1);
+  p.NCB = choose_ncb(N, p.n_slabs, mode, opts);
+  p.MODE = mode >= 0 ? mode : (p.NCB == 4 && M <= kGatherMaxM ? 0 : 1);
   // the gather mapping stages one 16-byte X chunk per lane: at most 4 rows
-  if (p.MODE == 0 && M > kGatherLimitM) return false;
-  p.n_strips = N / kTileN;
+  if (p.MODE == 0 && (M > kGatherLimitM || p.NCB != 4)) return false;
+  p.n_strips = N / (16 * p.NCB);
   p.T = K / kTileK;
   // the grid policy counts every row slab's workgroups
   const bool eight = sparse && p.MODE == 1 && !(opts & kOptFourWaves);
   const int units = p.n_strips * p.n_slabs;
   const int64_t U = int64_t(p.n_strips) * p.T;
-  if (!(opts & kOptStreamK) || split_k > 0) {
+  if (p.NCB == 2) {
+    // 32-column strips: no split unless there are fewer than 128 strips,
+    // eight waves per workgroup unless the strips have fewer than 8 tiles
+    int S = split_k;
+    if (S <= 0) {
+      S = 1;
+      while (int64_t(units) * S < 128 && 2 * S <= p.T / 8) S *= 2;
+    }
+    p.NW = (!(opts & kOptFourWaves) && p.T / S >= 8) ? 8 : 4;
+    S = std::max(S, (p.T + p.NW * 63 - 1) / (p.NW * 63));
+    p.S = std::max(1, std::min(S, p.T));
+    p.stream = 0;
+    p.G = p.n_strips * p.S;
+    p.C = p.S;
+  } else if (!(opts & kOptStreamK) || split_k > 0) {
     // uniform split-K: S ranges per strip, one workgroup each
     int S = split_k > 0 ? split_k : default_split(p.T, units, eight);
     // each wave indexes its tiles' group offsets from one register: <= 63 tiles
@@ -896,9 +1026,10 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   if (p.MODE == 0) {
     p.slot_bytes = align_up(size_t(p.slab_M) * kXStride * 2, 16);
   } else {
-    p.slot_bytes = sparse ? kImageBytes : 0;   // 16 B-operand blocks of 64 x 16 B
+    // 4 NCB B-operand blocks of 64 x 16 B
+    p.slot_bytes = sparse ? size_t(kImageBytes) / 4 * p.NCB : 0;
   }
-  const size_t red_bytes = size_t(p.NW) * p.slab_M * kTileN * 4;
+  const size_t red_bytes = size_t(p.NW) * p.slab_M * (16 * p.NCB) * 4;
   p.off_shc = align_up(std::max(p.NW * p.slot_bytes, red_bytes), 16);
   const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * p.slab_M * kTileN * 4 : 0;
   p.off_flag = align_up(p.off_shc + shc_bytes, 16);
@@ -906,8 +1037,8 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   p.lds_bytes = p.off_trash + 16;
   if (p.lds_bytes > 160 * 1024) return false;
 
-  // partial sums: [slab][strip][slot][row][64] fp32, every slab kSlabM rows apart
-  p.partial_bytes = p.C > 1 ? size_t(p.n_slabs) * p.n_strips * p.C * kSlabM * kTileN * 4 : 0;
+  // partial sums: [slab][strip][slot][row][strip width] fp32, every slab kSlabM rows apart
+  p.partial_bytes = p.C > 1 ? size_t(p.n_slabs) * p.n_strips * p.C * kSlabM * (16 * p.NCB) * 4 : 0;
   if (int64_t(p.n_slabs) * p.n_strips > kMaxStrips) return false;   // one counter each
   // every array is addressed with 32-bit byte offsets
   const size_t lim = size_t(1) << 31;
@@ -936,6 +1067,7 @@ int launch_matmul(const Plan& pl, const MatmulPtrs& p, bool dense, bool sparse, 
   a.N = pl.N;
   a.T = pl.T;
   a.S = pl.S;
+  a.G = pl.G;
   a.stream = pl.stream;
   a.C = pl.C;
   a.n_slabs = pl.n_slabs;

@@ -37,16 +37,16 @@ def c_params(**kw):
     return d
 
 
-def run(fq, prob, variant="fused", y="bf16", params=None, split_k=0, sparse="auto"):
+def run(fq, prob, variant="fused", y="bf16", params=None, split_k=0, sparse="auto", flags=0):
     X, Wq, s, z = fq.to_device(prob)
     if variant == "dense":
-        Y = fq.fq_w4a16_matmul(X, Wq, s, z, y_dtype=y, split_k=split_k)
+        Y = fq.fq_w4a16_matmul(X, Wq, s, z, y_dtype=y, split_k=split_k, flags=flags)
     else:
         tc = fq.TileCOODevice(fq.fq_pack_tile_coo(prob.K, prob.N, prob.k, prob.n, prob.v,
                                                   params))
         fn = fq.fq_w4a16_outlier_matmul if variant == "fused" else \
             fq.fq_w4a16_outlier_matmul_unfused
-        Y = fn(X, Wq, s, z, tc, y_dtype=y, split_k=split_k, sparse=sparse)
+        Y = fn(X, Wq, s, z, tc, y_dtype=y, split_k=split_k, sparse=sparse, flags=flags)
     torch.cuda.synchronize()
     if y == "bf16":
         return Y.view(torch.int16).cpu().numpy().view(np.uint16)
@@ -148,15 +148,17 @@ def test_exact_arithmetic_bit_exact(gpu_lib, case, variant, sparse):
     assert np.array_equal(y16, oracle.bf16_rne_bits(y_ref))
 
 
-SCHEDULE_FLAGS = {"stream_k": 4, "four_waves": 8, "stream_k+four_waves": 12}
+SCHEDULE_FLAGS = {"stream_k": 4, "four_waves": 8, "stream_k+four_waves": 12,
+                  "strip32": 16, "strip64": 32, "strip32+four_waves": 24,
+                  "strip64+four_waves": 40}
 
 
 @pytest.mark.parametrize("case", [c for c in EXACT_CASES if c[4] == 0],
                          ids=[f"exact{i}" for i, c in enumerate(EXACT_CASES) if c[4] == 0])
 @pytest.mark.parametrize("sched", list(SCHEDULE_FLAGS))
 def test_exact_schedules_bit_exact(gpu_lib, case, sched):
-    """The ablation schedules (Stream-K ranges, four waves only) give the
-    same exact result as the default one."""
+    """The ablation schedules (Stream-K ranges, four waves only) and both strip
+    widths (32 and 64 columns) give the same exact result as the default one."""
     M, K, N, frac, split_k, params = case
     log(f"exact schedule {sched} M={M} K={K} N={N} frac={frac}")
     fq = gpu_lib
@@ -170,6 +172,23 @@ def test_exact_schedules_bit_exact(gpu_lib, case, sched):
     y_ref = ref(prob).astype(np.float32)
     assert np.array_equal(y.cpu().numpy(), y_ref)
     assert np.array_equal(yu.cpu().numpy(), y_ref)
+
+
+@pytest.mark.parametrize("case", [c for c in EXACT_CASES if c[4] != 0],
+                         ids=[f"exact{i}" for i, c in enumerate(EXACT_CASES) if c[4] != 0])
+@pytest.mark.parametrize("strip", [16, 32], ids=["strip32", "strip64"])
+def test_exact_split_k_both_strip_widths(gpu_lib, case, strip):
+    """Explicit split-K (cross-workgroup partial sums) with 32- and 64-column
+    strips, fused, unfused and dense-only."""
+    M, K, N, frac, split_k, params = case
+    log(f"exact split strip flag={strip} M={M} K={K} N={N} split_k={split_k}")
+    prob = make_exact_problem(M, K, N, frac=frac, seed=M * 7 + K + N)
+    y_ref = ref(prob).astype(np.float32)
+    for variant in ("fused", "unfused"):
+        y = run(gpu_lib, prob, variant, "f32", params, split_k, "mfma", flags=strip)
+        assert np.array_equal(y, y_ref), variant
+    yd = run(gpu_lib, prob, "dense", "f32", split_k=split_k, flags=strip)
+    assert np.array_equal(yd, ref(prob, dense_only=True).astype(np.float32))
 
 
 def test_exact_dense_only(gpu_lib):
@@ -236,9 +255,11 @@ def test_workspace_counters_rearmed(gpu_lib):
 def test_workspace_shared_across_shapes(gpu_lib):
     """One workspace serving problems of different shapes in turn."""
     fq = gpu_lib
-    ws = torch.zeros(fq.fq_workspace_bytes(16, 4096, 4096), dtype=torch.uint8, device="cuda")
-    for (M, K, N, split_k) in [(16, 4096, 4096, 0), (3, 896, 320, 3), (1, 4096, 4096, 0),
-                               (5, 896, 192, 2), (16, 4096, 4096, 0)]:
+    shapes = [(16, 4096, 4096, 0), (3, 896, 320, 3), (1, 4096, 4096, 0), (5, 896, 192, 2),
+              (16, 4096, 4096, 0)]
+    ws = torch.zeros(max(fq.fq_workspace_bytes(M, K, N, split_k=sk) for M, K, N, sk in shapes),
+                     dtype=torch.uint8, device="cuda")
+    for (M, K, N, split_k) in shapes:
         prob = make_exact_problem(M, K, N, frac=0.02, seed=M + K + N)
         X, Wq, s, z = fq.to_device(prob)
         tc = fq.TileCOODevice(fq.fq_pack_tile_coo(K, N, prob.k, prob.n, prob.v))
@@ -256,22 +277,25 @@ FULL_SHAPES = [(4096, 6144), (4096, 4096), (4096, 28672), (14336, 4096)]
 
 @pytest.mark.parametrize("shape", FULL_SHAPES, ids=["qkv", "o", "gate_up", "down"])
 @pytest.mark.parametrize("M", [1, 16])
-def test_full_size_sampled_columns(gpu_lib, shape, M):
+@pytest.mark.parametrize("strip", [0, 16, 32], ids=["auto", "strip32", "strip64"])
+def test_full_size_sampled_columns(gpu_lib, shape, M, strip):
     """Llama-3-8B decode linears at full size, in the launch configuration the
-    benchmark times; the oracle computes a sample of columns one by one."""
+    benchmark times (auto) and with each strip width forced; the oracle
+    computes a sample of columns one by one."""
     K, N = shape
-    log(f"full K={K} N={N} M={M}")
+    log(f"full K={K} N={N} M={M} strip flag={strip}")
     prob = make_problem(M, K, N, frac=0.01, seed=seed_for(1, FULL_SHAPES.index(shape),
                                                            [1, 4, 8, 16].index(M)))
     rng = np.random.default_rng(K + N + M)
     cols = np.unique(np.concatenate([[0, 63, 64, N - 1], rng.choice(N, 192, replace=False)]))
     y_ref = ref(prob, cols)
-    y16 = run(gpu_lib, prob, "fused", "bf16")
+    sparse = "mfma" if strip == 16 else "auto"
+    y16 = run(gpu_lib, prob, "fused", "bf16", sparse=sparse, flags=strip)
     assert_bf16_close(y16[:, cols], y_ref)
-    y32 = run(gpu_lib, prob, "fused", "f32")
+    y32 = run(gpu_lib, prob, "fused", "f32", sparse=sparse, flags=strip)
     assert_f32_close(y32[:, cols], y_ref)
     # property that holds at any size: fused and unfused agree closely everywhere
-    yu = run(gpu_lib, prob, "unfused", "f32")
+    yu = run(gpu_lib, prob, "unfused", "f32", sparse=sparse, flags=strip)
     rel = np.linalg.norm(yu - y32) / np.linalg.norm(y32)
     assert rel <= F32_FROB
 

@@ -270,7 +270,10 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
     (dict(split_k=-1), "FQ_ERR_SHAPE"),
     (dict(flags=3), "FQ_ERR_UNSUPPORTED"),
     (dict(flags=1, M=5), "FQ_ERR_UNSUPPORTED"),
-    (dict(flags=16), "FQ_ERR_UNSUPPORTED"),
+    (dict(flags=64), "FQ_ERR_UNSUPPORTED"),
+    (dict(flags=16 | 32), "FQ_ERR_UNSUPPORTED"),   # both strip widths
+    (dict(flags=16 | 4), "FQ_ERR_UNSUPPORTED"),    # 32-column strips with Stream-K
+    (dict(flags=16 | 1), "FQ_ERR_UNSUPPORTED"),    # 32-column strips with the gather mapping
     (dict(flags=4 | 8 | 3), "FQ_ERR_UNSUPPORTED"),
     # 32-bit byte offsets: packed weights of 2^31 bytes, partial sums of 2^31 bytes
     (dict(K=131072, N=32768), "FQ_ERR_UNSUPPORTED"),
