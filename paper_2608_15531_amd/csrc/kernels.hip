@@ -90,12 +90,10 @@ constexpr int loads_per_tile() {
   return (DENSE ? 6 : 0) + (MODE == 0 ? 1 : 4 * MB) + (SPARSE ? 2 : 0);
 }
 
-// Tiles in flight per wave.  A 32-column tile takes half the code registers
-// of a 64-column one, which leaves room for four buffers with one 16-row
-// block; two 16-row blocks need twice the activation registers, which
-// leaves room for two buffers only.
+// Tiles in flight per wave.  Each buffer is one more copy of the tile code
+// in the loop body, so the depth stays at two.
 template <int MB, int NCB>
-constexpr int pipeline_depth() { return MB == 1 && NCB == 2 ? 4 : 2; }
+constexpr int pipeline_depth() { return 2; }
 
 // Packed-code words one lane loads per 32-row step: one word per 16-column
 // MFMA block of the strip (NCB blocks: 32-column strips load 8 bytes, 64-column
@@ -701,54 +699,39 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
     // D register buffers, all in flight: while tile t is computed from one,
     // the loads of tiles t+1 .. t+D-1 fill the others; when t is done its
     // buffer is refilled with tile t+D.  Every issue is unconditional (past the
-    // wave's last tile it re-reads that tile, which is still in cache), so each
-    // wait is exact: waiting for tile t leaves the (D-1) NL loads of the
-    // following tiles in flight.  The loop body handles D tiles and has a
-    // single back edge, so the compiler's own load tracking sees the same order
-    // on every entry; sched_barrier keeps the scheduler from sinking a tile's
-    // loads below the next wait, which would cut the prefetch depth.
+    // wave's last tile it re-reads that tile, which is still in cache), and
+    // every tile's loads go out in the same order -- dense, then Tile-COO
+    // groups -- from the first tile on, so the wait before each tile is the
+    // same exact count everywhere: the (D-1) NL loads of the following tiles
+    // stay in flight.  Only the first tile's group loads wait for
+    // tile_indptr, while its dense loads are already out.
+    //
+    // Code size is part of the cost: the instruction cache starts cold at
+    // every launch and each KB of code run for the first time costs about
+    // 0.4 us, so the loop body holds exactly one copy of the tile code per
+    // register buffer and the last partial round is predicated rather than
+    // peeled.
     constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
     constexpr int D = pipeline_depth<MB, NCB>();
     TileRegs<MB, MODE, NCB> rg[D];
     if (w_lo < w_hi) {
       const int last = w_hi - 1;
-      // The first tiles' dense loads go out before the group offsets have
-      // arrived; only the group loads wait for them.
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < D; ++i) {
-        load_tile_dense<MB, MODE, NCB, DENSE>(a, op, min(w_lo + i, last), n0, rg[i]);
+        issue(min(w_lo + i, last), rg[i]);
         __builtin_amdgcn_sched_barrier(0);
       }
-  #pragma unroll
-      for (int i = 0; i < D; ++i) {
-        issue_sparse(min(w_lo + i, last), rg[i]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      auto round = [&](int t) __attribute__((always_inline)) {
-  #pragma unroll
+      for (int t = w_lo; t < w_hi; t += D) {
+#pragma unroll
         for (int i = 0; i < D; ++i) {
-          wait_vmcnt<(D - 1) * NL>();
-          compute(rg[i]);
+          if (i == 0 || t + i < w_hi) {
+            wait_vmcnt<(D - 1) * NL>();
+            compute(rg[i]);
+          }
           issue(min(t + i + D, last), rg[i]);
           __builtin_amdgcn_sched_barrier(0);
         }
-      };
-      // The first round is peeled and the loop nested in it: the prologue's
-      // load order (all dense loads, then all group loads) differs from the
-      // steady state's, and the loop header must only be reached in the latter.
-      int t = w_lo;
-      if (t + D - 1 < w_hi) {
-        round(t);
-        for (t += D; t + D - 1 < w_hi; t += D) round(t);
       }
-      // fewer than D tiles left, all already loaded: no further issue
-      static_for<0, D - 1>([&](auto ic) {
-        constexpr int i = decltype(ic)::value;
-        if (t + i < w_hi) {
-          wait_vmcnt<(D - 2 - i) * NL>();
-          compute(rg[i]);
-        }
-      });
     }
     __syncthreads();
 
@@ -934,17 +917,32 @@ int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
   return (eight_waves && int64_t(n_strips) * S <= 256 && T / S >= 8) ? 8 : 4;
 }
 
-// Strip width.  32-column strips (128-byte segments of each packed row,
-// which stream as well as 256-byte ones) let a narrow matrix cover the GPU
-// without a cross-workgroup split, but cost about 1.5x the instructions per
-// byte (the activation permute, the per-tile epilogue and the outlier pass
-// are shared by half as many columns) and measured slower than 64-column
-// strips with split-K on every Llama-3 decode shape, so 64 is the default.
-int choose_ncb(int N, int n_slabs, int mode, int opts) {
-  (void)N;
-  (void)n_slabs;
-  (void)mode;
-  return (opts & kOptStrip32) ? 2 : 4;
+// The launch shape (strip width, split, waves per workgroup) the library
+// picks when the caller forces none.  Measured on MI355X over the Llama-3-8B
+// decode linears at M = 1..16 (graph replay, rotated weights):
+//  * N / 64 strips fill the GPU (gate+up): 64-column strips, no split.
+//  * Narrow N, K <= 8192 (qkv, o): 32-column strips (128-byte segments of
+//    each packed row, which stream as well as 256-byte ones) and no split,
+//    eight waves -- a cross-workgroup split-K reduction costs three
+//    dependent trips through the device-coherent memory level (about 2 us),
+//    more than the extra instructions per byte of the narrower strip.  With
+//    fewer than 192 strips and 12 or more rows the per-tile work is heavy
+//    enough that covering all CUs pays: split 2, four waves.
+//  * Narrow N, long K (down): 64-column strips split until there are about
+//    512 workgroups, four waves each.
+struct Shape {
+  int ncb, split, waves;   // split 0: the split-K default for that width
+};
+Shape default_shape(int T, int N, int n_slabs, int slab_M) {
+  const int64_t units64 = int64_t(N / 64) * n_slabs, units32 = int64_t(N / 32) * n_slabs;
+  if (units64 >= 256) return {4, 0, 0};
+  if (T <= 64) {
+    if (units32 < 192 && slab_M >= 12 && T >= 16) return {2, 2, 4};
+    return {2, 1, T >= 8 ? 8 : 4};
+  }
+  int S = 1;
+  while (units64 * S < 512 && 2 * S <= T / 8) S *= 2;
+  return {4, S, 4};
 }
 }  // namespace
 
@@ -962,24 +960,38 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   p.n_slabs = (M + kSlabM - 1) / kSlabM;
   p.slab_M = std::min(M, kSlabM);
   p.MB = p.slab_M <= 16 ? 1 : 2;
-  p.NCB = choose_ncb(N, p.n_slabs, mode, opts);
+  p.T = K / kTileK;
+  // strip width: forced, or 64 for the gather mapping and Stream-K, or the
+  // measured default
+  const bool forced = (opts & (kOptStrip32 | kOptStrip64 | kOptStreamK)) || mode == 0;
+  Shape shape = forced ? Shape{(opts & kOptStrip32) ? 2 : 4, 0, 0}
+                       : default_shape(p.T, N, p.n_slabs, p.slab_M);
+  if (split_k > 0) shape.split = split_k;
+  p.NCB = shape.ncb;
   p.MODE = mode >= 0 ? mode : (p.NCB == 4 && M <= kGatherMaxM ? 0 : 1);
   // the gather mapping stages one 16-byte X chunk per lane: at most 4 rows
   if (p.MODE == 0 && (M > kGatherLimitM || p.NCB != 4)) return false;
   p.n_strips = N / (16 * p.NCB);
-  p.T = K / kTileK;
   // the grid policy counts every row slab's workgroups
   const bool eight = sparse && p.MODE == 1 && !(opts & kOptFourWaves);
   const int units = p.n_strips * p.n_slabs;
   const int64_t U = int64_t(p.n_strips) * p.T;
-  if (p.NCB == 2) {
-    // 32-column strips: no split unless there are fewer than 128 strips,
-    // eight waves per workgroup unless the strips have fewer than 8 tiles
-    int S = split_k;
-    if (S <= 0) {
-      S = 1;
-      while (int64_t(units) * S < 128 && 2 * S <= p.T / 8) S *= 2;
-    }
+  if (shape.split > 0 && !(opts & kOptStreamK)) {
+    // an explicit split (the caller's or the default shape's)
+    int S = shape.split;
+    p.NW = shape.waves ? shape.waves : (p.NCB == 2 ? 8 : waves_per_workgroup(p.T, S, units, eight));
+    if ((opts & kOptFourWaves) || p.T / S < 8) p.NW = 4;
+    S = std::max(S, (p.T + p.NW * 63 - 1) / (p.NW * 63));
+    p.S = std::max(1, std::min(S, p.T));
+    p.stream = 0;
+    p.G = p.n_strips * p.S;
+    p.C = p.S;
+  } else if (p.NCB == 2) {
+    // 32-column strips forced, no split given: no split unless there are
+    // fewer than 128 strips, eight waves unless the strips have fewer than
+    // 8 tiles
+    int S = 1;
+    while (int64_t(units) * S < 128 && 2 * S <= p.T / 8) S *= 2;
     p.NW = (!(opts & kOptFourWaves) && p.T / S >= 8) ? 8 : 4;
     S = std::max(S, (p.T + p.NW * 63 - 1) / (p.NW * 63));
     p.S = std::max(1, std::min(S, p.T));
