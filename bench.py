@@ -107,10 +107,13 @@ def cpu_baseline(tilecoo_bytes: dict, budget_s: float = 20.0):
 
 
 def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
-    """Per-matmul graph-replay times of: the unfused two-kernel baseline; SD,
-    the fused kernel without the eight-wave workgroups and on an unreordered
-    Tile-COO; SD+EW, with eight-wave workgroups; SD+EW+RE, the default; and the
-    default with the Stream-K schedule.  Prints one JSON line."""
+    """Per-matmul graph-replay times of the paper's ablation steps (Sec. 5.5)
+    as this library implements them: the unfused two-kernel baseline; SD, the
+    fused kernel on an unreordered Tile-COO; SD+RE, with the column and element
+    reordering of Sec. 3.2.2 (the default configuration); SD+EW and SD+EW+RE,
+    the same with extra outlier waves beside the dense waves of each
+    workgroup (warp specialisation, FQ_SPARSE_WAVES); and the default with
+    the Stream-K schedule.  Prints one JSON line."""
     from synth import make_problem, seed_for
     # Tile-COO without reordering, one per shape, R copies
     plain = {}
@@ -121,18 +124,22 @@ def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
         host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v, prm)
         plain[name] = [fq.TileCOODevice(host, dev) for _ in range(R)]
     need_sk = max(fq.fq_workspace_bytes(c.M, c.K, c.N, flags=fq.FQ_SCHED_STREAM_K) for c in cases)
-    ws_sk = torch.zeros(max(need_sk, ws.numel()), dtype=torch.uint8, device=dev)
+    need_ew = max(fq.fq_workspace_bytes(c.M, c.K, c.N, flags=fq.FQ_SPARSE_WAVES) for c in cases)
+    ws_big = torch.zeros(max(need_sk, need_ew, ws.numel()), dtype=torch.uint8, device=dev)
+    EW = fq.FQ_SPARSE_WAVES
     variants = {
         "unfused": lambda c, r: fq.fq_w4a16_outlier_matmul_unfused(
             c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws),
         "SD": lambda c, r: fq.fq_w4a16_outlier_matmul(
-            c.X, *c.weights[r], plain[c.name][r], Y=c.Y, ws=ws, flags=fq.FQ_FOUR_WAVES),
-        "SD+EW": lambda c, r: fq.fq_w4a16_outlier_matmul(
             c.X, *c.weights[r], plain[c.name][r], Y=c.Y, ws=ws),
-        "SD+EW+RE": lambda c, r: fq.fq_w4a16_outlier_matmul(
+        "SD+RE": lambda c, r: fq.fq_w4a16_outlier_matmul(
             c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws),
-        "SD+EW+RE+StreamK": lambda c, r: fq.fq_w4a16_outlier_matmul(
-            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws_sk, flags=fq.FQ_SCHED_STREAM_K),
+        "SD+EW": lambda c, r: fq.fq_w4a16_outlier_matmul(
+            c.X, *c.weights[r], plain[c.name][r], Y=c.Y, ws=ws_big, flags=EW),
+        "SD+EW+RE": lambda c, r: fq.fq_w4a16_outlier_matmul(
+            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws_big, flags=EW),
+        "SD+RE+StreamK": lambda c, r: fq.fq_w4a16_outlier_matmul(
+            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws_big, flags=fq.FQ_SCHED_STREAM_K),
     }
 
     def capture(fn):
@@ -204,8 +211,8 @@ def main():
     ap.add_argument("--ablation", action="store_true",
                     help="no step timing: per-matmul times of the unfused baseline and of the "
                          "fused kernel with its techniques added one by one (SD: fused; EW: "
-                         "eight-wave workgroups; RE: Tile-COO reordering) and with Stream-K; "
-                         "prints one JSON line of geometric-mean speedups")
+                         "outlier waves beside the dense waves; RE: Tile-COO reordering) and "
+                         "with Stream-K; prints one JSON line of geometric-mean speedups")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="no timing: eager launches of the dominant kernel's matmuls over the "
                          "rotated copies, then a plain copy of COPY_CAL_BYTES, for rocprofv3 "

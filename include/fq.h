@@ -228,7 +228,7 @@ typedef struct {
  *   flags       bit set: one FQ_SPARSE_* value in bits 0-1 to force the
  *               sparse-path mapping (the library otherwise picks by M), and
  *               the schedule switches FQ_SCHED_STREAM_K, FQ_FOUR_WAVES,
- *               FQ_STRIP_32 and FQ_STRIP_64.
+ *               FQ_STRIP_32, FQ_STRIP_64 and FQ_SPARSE_WAVES.
  */
 typedef struct {
   int32_t M;
@@ -264,6 +264,17 @@ enum { FQ_SCHED_STREAM_K = 4, FQ_FOUR_WAVES = 8 };
  * reduction.  FQ_STRIP_32 (MFMA outlier mapping only, not with
  * FQ_SCHED_STREAM_K) and FQ_STRIP_64 force one width. */
 enum { FQ_STRIP_32 = 16, FQ_STRIP_64 = 32 };
+
+/* Warp specialisation (Sec. 3.1: dense and sparse warps in one CTA).
+ * FQ_SPARSE_WAVES adds outlier waves beside the dense waves of each
+ * workgroup of a fused launch with the MFMA outlier mapping and uniform
+ * split-K (half as many); the two kinds share the strip's K range and the
+ * output reduction, so the dense stream never waits for the Tile-COO
+ * groups.  By default every wave runs both paths for its own tiles, which
+ * measured faster on MI355X: the image-based outlier path costs about as
+ * much as the dense path when run alone, and interleaving the two in one
+ * wave hides their latencies better than splitting them. */
+enum { FQ_SPARSE_WAVES = 64 };
 
 /*
  * fq_workspace_bytes -- device workspace the matmul entry points need for

@@ -38,6 +38,7 @@ FQ_SCHED_STREAM_K = 4
 FQ_FOUR_WAVES = 8
 FQ_STRIP_32 = 16
 FQ_STRIP_64 = 32
+FQ_SPARSE_WAVES = 64
 
 
 class FqError(RuntimeError):

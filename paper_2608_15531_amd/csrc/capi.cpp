@@ -16,7 +16,8 @@ fq_status check_problem(const fq_problem* pr) {
   if (pr->group_size != fqi::kTileK) return FQ_ERR_UNSUPPORTED;
   if (pr->M > fqi::kMaxM) return FQ_ERR_UNSUPPORTED;
   if (pr->y_dtype != FQ_Y_BF16 && pr->y_dtype != FQ_Y_F32) return FQ_ERR_UNSUPPORTED;
-  if (pr->flags & ~(FQ_SPARSE_MASK | FQ_SCHED_STREAM_K | FQ_FOUR_WAVES | FQ_STRIP_32 | FQ_STRIP_64))
+  if (pr->flags & ~(FQ_SPARSE_MASK | FQ_SCHED_STREAM_K | FQ_FOUR_WAVES | FQ_STRIP_32 | FQ_STRIP_64 |
+                    FQ_SPARSE_WAVES))
     return FQ_ERR_UNSUPPORTED;
   const int mapping = pr->flags & FQ_SPARSE_MASK;
   if ((pr->flags & FQ_STRIP_32) &&
@@ -90,7 +91,8 @@ int plan_opts(const fq_problem* pr) {
   return ((pr->flags & FQ_SCHED_STREAM_K) ? fqi::kOptStreamK : 0) |
          ((pr->flags & FQ_FOUR_WAVES) ? fqi::kOptFourWaves : 0) |
          ((pr->flags & FQ_STRIP_32) ? fqi::kOptStrip32 : 0) |
-         ((pr->flags & FQ_STRIP_64) ? fqi::kOptStrip64 : 0);
+         ((pr->flags & FQ_STRIP_64) ? fqi::kOptStrip64 : 0) |
+         ((pr->flags & FQ_SPARSE_WAVES) ? fqi::kOptSparseWaves : 0);
 }
 
 }  // namespace

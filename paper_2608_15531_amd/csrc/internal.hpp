@@ -35,7 +35,8 @@ struct Plan {
   int n_strips;      // N / (16 NCB)
   int T;             // tiles per strip, K / 128
   int S;             // K ranges per strip (explicit split-K); 1 under Stream-K
-  int NW;            // waves per workgroup: 4 or 8
+  int NW;            // dense (or dense and outlier) waves per workgroup: 4 or 8
+  int NWS;           // outlier waves beside them (warp specialisation), 0 or NW / 2
   int stream;        // 1: Stream-K schedule, 0: uniform split-K
   int G;             // workgroups per slab
   int C;             // partial-sum slots per strip (most contributors to one strip)
@@ -52,6 +53,7 @@ constexpr int kOptStreamK = 1;     // Stream-K ranges instead of uniform split-K
 constexpr int kOptFourWaves = 2;   // never eight waves per workgroup
 constexpr int kOptStrip32 = 4;     // 32-column strips (MFMA outlier mapping, no Stream-K)
 constexpr int kOptStrip64 = 8;     // 64-column strips
+constexpr int kOptSparseWaves = 16;   // warp specialisation: outlier waves beside the dense waves
 
 // Returns false when (M, K, N) is outside what the kernels implement.
 // mode: -1 picks the sparse mapping by M, 0 forces gathers, 1 forces MFMA.

@@ -363,15 +363,21 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
   for (int j = 0; j < 4; ++j) lds_store16(addr[j], 0u);
 }
 
-template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK>
-__global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
+template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS>
+__global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args) {
   static_assert(NCB == 4 || (NCB == 2 && MODE == 1), "32-column strips use the MFMA outlier mapping");
+  // NWS > 0: warp specialisation (Sec. 3.1) -- NW dense waves and NWS outlier
+  // waves share the strip's K range and the output reduction.
+  constexpr int NT = NW + NWS;                 // waves per workgroup
+  constexpr bool WS = NWS > 0;
+  static_assert(!WS || (KD && KS && MODE == 1 && !SK), "outlier waves: fused MFMA mapping, split-K");
   constexpr int NC = 16 * NCB;                 // strip width, columns
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // wave-uniform: keeps the tile loop in scalar control flow
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool swave = WS && wave >= NW;         // an outlier wave
   const int h = lane >> 4;                     // k-chunk of the MFMA operands
   const int c4 = lane & 15;                    // MFMA column / A row
 
@@ -425,10 +431,11 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
     u_end = int64_t(wg + 1) * U / G;
   }
 
-  unsigned char* slot = smem + size_t(wave) * a.slot_bytes;
+  // LDS slots: one per wave, or one per outlier wave under specialisation
+  unsigned char* slot = smem + size_t(WS ? (swave ? wave - NW : 0) : wave) * a.slot_bytes;
   uint16_t* xs = reinterpret_cast<uint16_t*>(slot);   // MODE 0: X slice
   uint16_t* bo = reinterpret_cast<uint16_t*>(slot);   // MODE 1: B-operand image
-  static_assert(MODE != 1 || !SPARSE || fqi::kImageBytes == 16384, "image layout");
+  static_assert(MODE != 1 || !KS || fqi::kImageBytes == 16384, "image layout");
   constexpr int kImageBlocks = 4 * NCB;        // 1 KB MFMA B-operand blocks per image
   // Each wave owns its sparse output buffer (gather mode): within a wave the
   // LDS unit applies adds in a fixed order, so repeated calls are identical.
@@ -468,170 +475,213 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
   uint32_t tp = 0;
   f32x4_t acc[MB][NCB];
 
-  auto issue_sparse = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
-    uint32_t g0 = 0, g1 = 0;
-    if (SPARSE) {
-      const uint32_t ng = uint32_t(a.n_groups);   // < 2^27, checked on the host
-      g0 = min(uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo)), ng);
-      g1 = max(g0, min(uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo + 1)), ng));
-    }
-    load_tile_sparse<MB, MODE, NCB, SPARSE>(op, lane, g0, g1, r);
-  };
-  auto issue = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
-    load_tile_dense<MB, MODE, NCB, DENSE>(a, op, t, n0, r);
-    issue_sparse(t, r);
-  };
+  // The tile pipeline of one wave for one role: dense and outlier work
+  // (every wave without specialisation), or one of them.
+  auto tiles = [&](auto rd_c, auto rs_c) __attribute__((always_inline)) {
+    constexpr bool DENSE = decltype(rd_c)::value;
+    constexpr bool SPARSE = decltype(rs_c)::value;
+    auto issue_sparse = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
+      uint32_t g0 = 0, g1 = 0;
+      if (SPARSE) {
+        const uint32_t ng = uint32_t(a.n_groups);   // < 2^27, checked on the host
+        g0 = min(uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo)), ng);
+        g1 = max(g0, min(uint32_t(__builtin_amdgcn_readlane(int(tp), t - w_lo + 1)), ng));
+      }
+      load_tile_sparse<MB, MODE, NCB, SPARSE>(op, lane, g0, g1, r);
+    };
+    auto issue = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
+      load_tile_dense<MB, MODE, NCB, DENSE>(a, op, t, n0, r);
+      issue_sparse(t, r);
+    };
 
-  auto compute = [&](const TileRegs<MB, MODE, NCB>& cur) __attribute__((always_inline)) {
-    // ---- X fragments
-    bf16x8_t A[MB][4];
-    if (MODE == 0) {
-      // stage the slice (lanes past the last row rewrite row M-1 with the
-      // same values, which keeps the store unconditional), then read it back
-      // in MFMA operand order
-      const int m = min(lane >> 4, a.M - 1);
-      *reinterpret_cast<uint4*>(xs + m * XS + 8 * (lane & 15)) = permute_chunk(cur.x[0]);
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int step = 0; step < 4; ++step)
-        A[0][step] = *reinterpret_cast<const bf16x8_t*>(xs + min(c4, a.M - 1) * XS + step * 32 + 8 * h);
-    } else {
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
+    auto compute = [&](const TileRegs<MB, MODE, NCB>& cur) __attribute__((always_inline)) {
+      // ---- X fragments
+      bf16x8_t A[MB][4];
+      if (MODE == 0) {
+        // stage the slice (lanes past the last row rewrite row M-1 with the
+        // same values, which keeps the store unconditional), then read it back
+        // in MFMA operand order
+        const int m = min(lane >> 4, a.M - 1);
+        *reinterpret_cast<uint4*>(xs + m * XS + 8 * (lane & 15)) = permute_chunk(cur.x[0]);
+        __builtin_amdgcn_wave_barrier();
+  #pragma unroll
         for (int step = 0; step < 4; ++step)
-          A[mb][step] = __builtin_bit_cast(bf16x8_t, permute_chunk(cur.x[mb * 4 + step]));
-    }
-
-    // ---- dense path: per 32-row step, dequantise the lane's words and
-    // multiply; one more MFMA against ones gives the rows' sums of X.  It
-    // comes first so that a tile's dense work never waits for its Tile-COO
-    // groups, whose loads depend on tile_indptr and are issued last.
-    constexpr bool SPM = SPARSE && MODE == 1;
-    f32x4_t tmp[MB][NCB], xsum[MB];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      xsum[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < NCB; ++c) tmp[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    }
-    if (DENSE) {
-#pragma unroll
-      for (int step = 0; step < 4; ++step) {
-        uint32_t w4[NCB];
-        if constexpr (NCB == 4) {
-          w4[0] = cur.w[step].x; w4[1] = cur.w[step].y; w4[2] = cur.w[step].z; w4[3] = cur.w[step].w;
-        } else {
-          w4[0] = cur.w[step].x; w4[1] = cur.w[step].y;
-        }
-#pragma unroll
-        for (int c = 0; c < NCB; ++c) {
-          const bf16x8_t Bq = dequant_word(w4[c]);
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
-            tmp[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bq, tmp[mb][c], 0, 0, 0);
-        }
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-          xsum[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], ones, xsum[mb], 0, 0, 0);
-      }
-    }
-
-    // ---- dense epilogue: eq. (3) once per (group, column) in fp32.  Rows
-    // 4h + r with r >= M (M < 4) never reach the output: skip them.
-    if (DENSE) {
-      float sc[NCB], zf[NCB];
-      if constexpr (NCB == 4) {
-        sc[0] = f16_bits_to_f32(cur.s.x & 0xFFFFu);
-        sc[1] = f16_bits_to_f32(cur.s.x >> 16);
-        sc[2] = f16_bits_to_f32(cur.s.y & 0xFFFFu);
-        sc[3] = f16_bits_to_f32(cur.s.y >> 16);
+          A[0][step] = *reinterpret_cast<const bf16x8_t*>(xs + min(c4, a.M - 1) * XS + step * 32 + 8 * h);
       } else {
-        sc[0] = f16_bits_to_f32(cur.s & 0xFFFFu);
-        sc[1] = f16_bits_to_f32(cur.s >> 16);
+  #pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+  #pragma unroll
+          for (int step = 0; step < 4; ++step)
+            A[mb][step] = __builtin_bit_cast(bf16x8_t, permute_chunk(cur.x[mb * 4 + step]));
       }
-      // the lane's columns n0 + NCB*c4 + c sit at nibbles (NCB*c4) % 8 + c of the word
-      const int zsh = ((NCB * c4) & 7) * 4;
-#pragma unroll
-      for (int c = 0; c < NCB; ++c) zf[c] = kCodeOffset + float((cur.z >> (zsh + 4 * c)) & 15u);
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if (MB == 1 && r > 0 && r >= a.M) break;
-#pragma unroll
-          for (int c = 0; c < NCB; ++c)
-            acc[mb][c][r] += sc[c] * (tmp[mb][c][r] - zf[c] * xsum[mb][r]);
-        }
-    }
 
-    // ---- sparse path, MFMA mapping: scatter the tile's outliers into the
-    // image, read it back per step and multiply into the output tile
-    uint32_t n_g = 0;
-    if (SPARSE) n_g = cur.g1 - cur.g0;
-    uint32_t addr[2][4];
-    if (SPM) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        if (uint32_t(lane + 64 * j) < n_g) scatter_group<NCB>(img, trash, cur.g[j], half, addr[j]);
-      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
-        uint32_t ad[4];
-        scatter_group<NCB>(img, trash, a.packed[cur.g0 + gi], half, ad);
+      // ---- dense path: per 32-row step, dequantise the lane's words and
+      // multiply; one more MFMA against ones gives the rows' sums of X.  It
+      // comes first so that a tile's dense work never waits for its Tile-COO
+      // groups, whose loads depend on tile_indptr and are issued last.
+      constexpr bool SPM = SPARSE && MODE == 1;
+      f32x4_t tmp[MB][NCB], xsum[MB];
+  #pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        xsum[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  #pragma unroll
+        for (int c = 0; c < NCB; ++c) tmp[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       }
-      __builtin_amdgcn_wave_barrier();
-      const uint4* b4 = reinterpret_cast<const uint4*>(bo);
-#pragma unroll
-      for (int step = 0; step < 4; ++step) {
-        bf16x8_t Bo[NCB];
-#pragma unroll
-        for (int c = 0; c < NCB; ++c) Bo[c] = __builtin_bit_cast(bf16x8_t, b4[(step * NCB + c) * 64 + lane]);
-#pragma unroll
-        for (int c = 0; c < NCB; ++c)
-#pragma unroll
+      if (DENSE) {
+  #pragma unroll
+        for (int step = 0; step < 4; ++step) {
+          uint32_t w4[NCB];
+          if constexpr (NCB == 4) {
+            w4[0] = cur.w[step].x; w4[1] = cur.w[step].y; w4[2] = cur.w[step].z; w4[3] = cur.w[step].w;
+          } else {
+            w4[0] = cur.w[step].x; w4[1] = cur.w[step].y;
+          }
+  #pragma unroll
+          for (int c = 0; c < NCB; ++c) {
+            const bf16x8_t Bq = dequant_word(w4[c]);
+  #pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+              tmp[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bq, tmp[mb][c], 0, 0, 0);
+          }
+  #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
-            acc[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bo[c], acc[mb][c], 0, 0, 0);
+            xsum[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], ones, xsum[mb], 0, 0, 0);
+        }
       }
-    }
 
-    // ---- gather mapping: the first two groups' X values from the staged slice
-    Gathered gx[2];
-    bool gsingle[2] = {false, false};
-    if (SPARSE && MODE == 0) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        gsingle[j] = uint32_t(lane + 64 * j) < n_g && single_column(decode_group(cur.g[j]));
-        if (gsingle[j]) gather_x(a, xs, cur.g[j], gx[j]);
+      // ---- dense epilogue: eq. (3) once per (group, column) in fp32.  Rows
+      // 4h + r with r >= M (M < 4) never reach the output: skip them.
+      if (DENSE) {
+        float sc[NCB], zf[NCB];
+        if constexpr (NCB == 4) {
+          sc[0] = f16_bits_to_f32(cur.s.x & 0xFFFFu);
+          sc[1] = f16_bits_to_f32(cur.s.x >> 16);
+          sc[2] = f16_bits_to_f32(cur.s.y & 0xFFFFu);
+          sc[3] = f16_bits_to_f32(cur.s.y >> 16);
+        } else {
+          sc[0] = f16_bits_to_f32(cur.s & 0xFFFFu);
+          sc[1] = f16_bits_to_f32(cur.s >> 16);
+        }
+        // the lane's columns n0 + NCB*c4 + c sit at nibbles (NCB*c4) % 8 + c of the word
+        const int zsh = ((NCB * c4) & 7) * 4;
+  #pragma unroll
+        for (int c = 0; c < NCB; ++c) zf[c] = kCodeOffset + float((cur.z >> (zsh + 4 * c)) & 15u);
+  #pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+  #pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if (MB == 1 && r > 0 && r >= a.M) break;
+  #pragma unroll
+            for (int c = 0; c < NCB; ++c)
+              acc[mb][c][r] += sc[c] * (tmp[mb][c][r] - zf[c] * xsum[mb][r]);
+          }
       }
-    }
 
-    // ---- MFMA mapping: restore the zeros of the image
-    if (SPM) {
+      // ---- sparse path, MFMA mapping: scatter the tile's outliers into the
+      // image, read it back per step and multiply into the output tile
+      uint32_t n_g = 0;
+      if (SPARSE) n_g = cur.g1 - cur.g0;
+      uint32_t addr[2][4];
+      if (SPM) {
+  #pragma unroll
+        for (int j = 0; j < 2; ++j)
+          if (uint32_t(lane + 64 * j) < n_g) scatter_group<NCB>(img, trash, cur.g[j], half, addr[j]);
+        for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
+          uint32_t ad[4];
+          scatter_group<NCB>(img, trash, a.packed[cur.g0 + gi], half, ad);
+        }
+        __builtin_amdgcn_wave_barrier();
+        const uint4* b4 = reinterpret_cast<const uint4*>(bo);
+  #pragma unroll
+        for (int step = 0; step < 4; ++step) {
+          bf16x8_t Bo[NCB];
+  #pragma unroll
+          for (int c = 0; c < NCB; ++c) Bo[c] = __builtin_bit_cast(bf16x8_t, b4[(step * NCB + c) * 64 + lane]);
+  #pragma unroll
+          for (int c = 0; c < NCB; ++c)
+  #pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+              acc[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bo[c], acc[mb][c], 0, 0, 0);
+        }
+      }
+
+      // ---- gather mapping: the first two groups' X values from the staged slice
+      Gathered gx[2];
+      bool gsingle[2] = {false, false};
+      if (SPARSE && MODE == 0) {
+  #pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          gsingle[j] = uint32_t(lane + 64 * j) < n_g && single_column(decode_group(cur.g[j]));
+          if (gsingle[j]) gather_x(a, xs, cur.g[j], gx[j]);
+        }
+      }
+
+      // ---- MFMA mapping: restore the zeros of the image
+      if (SPM) {
+        __builtin_amdgcn_wave_barrier();
+  #pragma unroll
+        for (int j = 0; j < 2; ++j)
+          if (uint32_t(lane + 64 * j) < n_g) clear_group(addr[j]);
+        for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
+          uint32_t o01, o23;
+          const uint4 raw = a.packed[cur.g0 + gi];
+          image_offsets<NCB>(raw.x, raw.y, o01, o23);
+          const uint32_t ad[4] = {img + (o01 & 0xFFFFu), img + (o01 >> 16), img + (o23 & 0xFFFFu),
+                                  img + (o23 >> 16)};
+          clear_group(ad);   // zeros everywhere the group could have written
+        }
+      }
+      // ---- gather mapping: finish the first two groups, then any further ones
+      if (SPARSE && MODE == 0) {
+  #pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          if (gsingle[j]) gather_add(a, cur.g[j], gx[j], shc);
+          else if (uint32_t(lane + 64 * j) < n_g) sparse_gather(a, xs, cur.g[j], shc);
+        }
+        for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
+          sparse_gather(a, xs, a.packed[cur.g0 + gi], shc);
+      }
       __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        if (uint32_t(lane + 64 * j) < n_g) clear_group(addr[j]);
-      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
-        uint32_t o01, o23;
-        const uint4 raw = a.packed[cur.g0 + gi];
-        image_offsets<NCB>(raw.x, raw.y, o01, o23);
-        const uint32_t ad[4] = {img + (o01 & 0xFFFFu), img + (o01 >> 16), img + (o23 & 0xFFFFu),
-                                img + (o23 >> 16)};
-        clear_group(ad);   // zeros everywhere the group could have written
-      }
-    }
-    // ---- gather mapping: finish the first two groups, then any further ones
-    if (SPARSE && MODE == 0) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        if (gsingle[j]) gather_add(a, cur.g[j], gx[j], shc);
-        else if (uint32_t(lane + 64 * j) < n_g) sparse_gather(a, xs, cur.g[j], shc);
-      }
-      for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
-        sparse_gather(a, xs, a.packed[cur.g0 + gi], shc);
-    }
-    __builtin_amdgcn_wave_barrier();
-  };
+    };
 
+    // D register buffers, all in flight: while tile t is computed from one,
+    // the loads of tiles t+1 .. t+D-1 fill the others; when t is done its
+    // buffer is refilled with tile t+D.  Every issue is unconditional (past
+    // the wave's last tile it re-reads that tile, which is still in cache),
+    // and every tile's loads go out in the same order -- dense, then Tile-COO
+    // groups -- from the first tile on, so the wait before each tile is the
+    // same exact count everywhere: the (D-1) NL loads of the following tiles
+    // stay in flight.  Only the first tile's group loads wait for
+    // tile_indptr, while its dense loads are already out.
+    //
+    // Code size is part of the cost: the instruction cache starts cold at
+    // every launch and each KB of code run for the first time costs about
+    // 0.4 us, so the loop body holds exactly one copy of the tile code per
+    // register buffer and the last partial round is predicated rather than
+    // peeled.
+    constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
+    constexpr int D = pipeline_depth<MB, NCB>();
+    TileRegs<MB, MODE, NCB> rg[D];
+    if (w_lo < w_hi) {
+      const int last = w_hi - 1;
+#pragma unroll
+      for (int i = 0; i < D; ++i) {
+        issue(min(w_lo + i, last), rg[i]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      for (int t = w_lo; t < w_hi; t += D) {
+#pragma unroll
+        for (int i = 0; i < D; ++i) {
+          if (i == 0 || t + i < w_hi) {
+            wait_vmcnt<(D - 1) * NL>();
+            compute(rg[i]);
+          }
+          issue(min(t + i + D, last), rg[i]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+  };
 
   // Partial sums cross workgroups through device-coherent (sc1) 16-byte
   // accesses, the encoding of relaxed agent-scope atomics; no cache-wide
@@ -670,17 +720,20 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
     t_lo = __builtin_amdgcn_readfirstlane(t_lo);
     t_hi = __builtin_amdgcn_readfirstlane(t_hi);
     const uint32_t nt = uint32_t(t_hi - t_lo);
-    w_lo = t_lo + int(nt * uint32_t(wave) / NW);    // this wave's tiles [w_lo, w_hi)
-    w_hi = t_lo + int(nt * uint32_t(wave + 1) / NW);
+    // this wave's tiles [w_lo, w_hi): an even share among the waves of its role
+    const uint32_t rw = uint32_t(swave ? wave - NW : wave), rn = swave ? NWS : NW;
+    w_lo = t_lo + int(nt * rw / rn);
+    w_hi = t_lo + int(nt * (rw + 1) / rn);
     n0 = strip * NC;
     // Tile-COO tiles are 128 x 64 and stored strip-major: a 32-column strip
     // reads the tiles of its 64-column strip and keeps its half's columns
     tile_base = int64_t(uint32_t(NCB == 4 ? strip : strip >> 1) * uint32_t(a.T));
     half = NCB == 4 ? 0u : uint32_t(strip & 1);
 
-    if (SPARSE && MODE == 0)
+    const bool has_sparse = KS && (!WS || swave);
+    if (KS && MODE == 0)
       for (int i = lane; i < a.M * 64; i += 64) shc[i] = 0.f;
-    if (SPARSE && MODE == 1) {
+    if (KS && MODE == 1 && has_sparse) {
       uint4* b4 = reinterpret_cast<uint4*>(bo);
 #pragma unroll
       for (int i = 0; i < kImageBlocks; ++i) b4[i * 64 + lane] = uint4{0u, 0u, 0u, 0u};
@@ -689,49 +742,18 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
     // The value is used raw (clamped only when read) so that nothing waits
     // for it before the first tiles' dense loads are out.
     tp = 0;
-    if (SPARSE && lane <= w_hi - w_lo) tp = a.tile_indptr[tile_base + w_lo + lane];
+    if (has_sparse && lane <= w_hi - w_lo) tp = a.tile_indptr[tile_base + w_lo + lane];
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int c = 0; c < NCB; ++c) acc[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // D register buffers, all in flight: while tile t is computed from one,
-    // the loads of tiles t+1 .. t+D-1 fill the others; when t is done its
-    // buffer is refilled with tile t+D.  Every issue is unconditional (past the
-    // wave's last tile it re-reads that tile, which is still in cache), and
-    // every tile's loads go out in the same order -- dense, then Tile-COO
-    // groups -- from the first tile on, so the wait before each tile is the
-    // same exact count everywhere: the (D-1) NL loads of the following tiles
-    // stay in flight.  Only the first tile's group loads wait for
-    // tile_indptr, while its dense loads are already out.
-    //
-    // Code size is part of the cost: the instruction cache starts cold at
-    // every launch and each KB of code run for the first time costs about
-    // 0.4 us, so the loop body holds exactly one copy of the tile code per
-    // register buffer and the last partial round is predicated rather than
-    // peeled.
-    constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
-    constexpr int D = pipeline_depth<MB, NCB>();
-    TileRegs<MB, MODE, NCB> rg[D];
-    if (w_lo < w_hi) {
-      const int last = w_hi - 1;
-#pragma unroll
-      for (int i = 0; i < D; ++i) {
-        issue(min(w_lo + i, last), rg[i]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      for (int t = w_lo; t < w_hi; t += D) {
-#pragma unroll
-        for (int i = 0; i < D; ++i) {
-          if (i == 0 || t + i < w_hi) {
-            wait_vmcnt<(D - 1) * NL>();
-            compute(rg[i]);
-          }
-          issue(min(t + i + D, last), rg[i]);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
+    if constexpr (WS) {
+      if (swave) tiles(std::false_type{}, std::true_type{});
+      else tiles(std::true_type{}, std::false_type{});
+    } else {
+      tiles(std::integral_constant<bool, KD>{}, std::integral_constant<bool, KS>{});
     }
     __syncthreads();
 
@@ -756,14 +778,14 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
     const bool shared = n_contrib > 1;
     const uint32_t row_bytes = 4u * NC;
     const uint32_t strip_part = uint32_t(strip) * uint32_t(a.C) * uint32_t(a.M) * row_bytes;
-    for (int i = tid; i < a.M * QPR; i += 64 * NW) {
+    for (int i = tid; i < a.M * QPR; i += 64 * NT) {
       const int m = i / QPR;
       const int cq = i - m * QPR;
       f32x4_t v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int w = 0; w < NW; ++w)
+      for (int w = 0; w < NT; ++w)
         v += *reinterpret_cast<const f32x4_t*>(red + (w * a.M + m) * NC + 4 * cq);
-      if (SPARSE && MODE == 0) {
+      if (KS && MODE == 0) {
 #pragma unroll
         for (int w = 0; w < NW; ++w)
           v += *reinterpret_cast<const f32x4_t*>(shc_all + (w * a.M + m) * 64 + 4 * cq);
@@ -788,7 +810,7 @@ __global__ void __launch_bounds__(64 * NW) matmul_kernel(MatmulArgs args) {
         // The last contributor adds the partials in contributor order, with
         // up to eight loads in flight per thread.
         constexpr int kBatch = 8;
-        for (int i = tid; i < a.M * QPR; i += 64 * NW) {
+        for (int i = tid; i < a.M * QPR; i += 64 * NT) {
           const int m = i / QPR;
           const int cq = i - m * QPR;
           const uint32_t base = strip_part + uint32_t(m) * row_bytes + uint32_t(cq) * 16u;
@@ -842,9 +864,9 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
   }
 }
 
-template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK>
+template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK, int NWS = 0>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK>;
+  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS>;
   if (pl.lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -852,12 +874,15 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
     if (e != hipSuccess) return int(e);
   }
   const unsigned grid = unsigned(pl.G) * unsigned(pl.n_slabs);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * NW), pl.lds_bytes, stream, args);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * (NW + NWS)), pl.lds_bytes, stream, args);
   return int(hipGetLastError());
 }
 
 template <int MB, int MODE, int NCB, int NW, bool SK>
 int launch_sched(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
+  if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8)) {
+    if (dense && sparse && pl.NWS > 0) return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2>(pl, a, s);
+  }
   if (dense && sparse) return launch_variant<MB, MODE, NCB, true, true, NW, SK>(pl, a, s);
   if (dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK>(pl, a, s);
   return launch_variant<MB, MODE, NCB, false, true, NW, SK>(pl, a, s);
@@ -1034,6 +1059,13 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
     p.C = C;
   }
   p.B = sparse ? B : 1;
+  // warp specialisation on request: NW / 2 outlier waves beside the NW
+  // dense waves of a fused launch with the MFMA outlier mapping and uniform
+  // split-K
+  p.NWS = (dense && sparse && p.MODE == 1 && !p.stream && (opts & kOptSparseWaves)) ? p.NW / 2 : 0;
+  // twelve waves of 64-column tiles with two 16-row blocks exceed the
+  // registers of three waves per SIMD
+  if (p.NCB == 4 && p.MB == 2 && p.NW == 8) p.NWS = 0;
 
   if (p.MODE == 0) {
     p.slot_bytes = align_up(size_t(p.slab_M) * kXStride * 2, 16);
@@ -1041,8 +1073,11 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
     // 4 NCB B-operand blocks of 64 x 16 B
     p.slot_bytes = sparse ? size_t(kImageBytes) / 4 * p.NCB : 0;
   }
-  const size_t red_bytes = size_t(p.NW) * p.slab_M * (16 * p.NCB) * 4;
-  p.off_shc = align_up(std::max(p.NW * p.slot_bytes, red_bytes), 16);
+  // slots: one per wave, or one per outlier wave under specialisation; the
+  // reduction buffer (one tile per wave) reuses them
+  const int n_slots = p.NWS > 0 ? p.NWS : p.NW;
+  const size_t red_bytes = size_t(p.NW + p.NWS) * p.slab_M * (16 * p.NCB) * 4;
+  p.off_shc = align_up(std::max(n_slots * p.slot_bytes, red_bytes), 16);
   const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * p.slab_M * kTileN * 4 : 0;
   p.off_flag = align_up(p.off_shc + shc_bytes, 16);
   p.off_trash = p.off_flag + 16;

@@ -150,15 +150,18 @@ def test_exact_arithmetic_bit_exact(gpu_lib, case, variant, sparse):
 
 SCHEDULE_FLAGS = {"stream_k": 4, "four_waves": 8, "stream_k+four_waves": 12,
                   "strip32": 16, "strip64": 32, "strip32+four_waves": 24,
-                  "strip64+four_waves": 40}
+                  "strip64+four_waves": 40, "sparse_waves": 64,
+                  "strip32+sparse_waves": 80, "strip64+sparse_waves": 96,
+                  "four_waves+sparse_waves": 72}
 
 
 @pytest.mark.parametrize("case", [c for c in EXACT_CASES if c[4] == 0],
                          ids=[f"exact{i}" for i, c in enumerate(EXACT_CASES) if c[4] == 0])
 @pytest.mark.parametrize("sched", list(SCHEDULE_FLAGS))
 def test_exact_schedules_bit_exact(gpu_lib, case, sched):
-    """The ablation schedules (Stream-K ranges, four waves only) and both strip
-    widths (32 and 64 columns) give the same exact result as the default one."""
+    """The ablation schedules (Stream-K ranges, four waves only, outlier
+    waves beside the dense waves) and both strip widths (32 and 64 columns) give the same exact
+    result as the default one."""
     M, K, N, frac, split_k, params = case
     log(f"exact schedule {sched} M={M} K={K} N={N} frac={frac}")
     fq = gpu_lib

@@ -270,7 +270,7 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
     (dict(split_k=-1), "FQ_ERR_SHAPE"),
     (dict(flags=3), "FQ_ERR_UNSUPPORTED"),
     (dict(flags=1, M=5), "FQ_ERR_UNSUPPORTED"),
-    (dict(flags=64), "FQ_ERR_UNSUPPORTED"),
+    (dict(flags=128), "FQ_ERR_UNSUPPORTED"),
     (dict(flags=16 | 32), "FQ_ERR_UNSUPPORTED"),   # both strip widths
     (dict(flags=16 | 4), "FQ_ERR_UNSUPPORTED"),    # 32-column strips with Stream-K
     (dict(flags=16 | 1), "FQ_ERR_UNSUPPORTED"),    # 32-column strips with the gather mapping
