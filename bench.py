@@ -37,9 +37,28 @@ SHAPES = [("qkv", 4096, 6144), ("o", 4096, 4096), ("gate_up", 4096, 28672),
           ("down", 14336, 4096)]
 MS = [1, 4, 8, 16]
 FRAC = 0.01
-DOMINANT_MIN_M = 4          # the step's M >= 4 matmuls: fused kernel, MFMA sparse mapping
 COPY_CAL_BYTES = 256 << 20  # plain device copy used to calibrate FETCH_SIZE / WRITE_SIZE
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fused_llama3_8b_decode_traffic.md")
+
+
+def kernel_name(fq, M, K, N):
+    """Template instance of the fused kernel the library launches for (M, K, N)."""
+    c = fq.fq_launch_config(M, K, N)
+    mb = 1 if min(M, 32) <= 16 else 2
+    mode = 0 if c["mapping"] == "gather" else 1
+    sk = "true" if c["stream_k"] else "false"
+    return (f"matmul_kernel<{mb}, {mode}, {c['strip_cols'] // 16}, true, true, "
+            f"{c['dense_waves']}, {sk}, {c['outlier_waves']}>")
+
+
+def dominant_kernel(fq, cases):
+    """The kernel instance that takes most of the step, and its cases."""
+    groups = {}
+    for c in cases:
+        groups.setdefault(kernel_name(fq, c.M, c.K, c.N), []).append(c)
+    # weigh each instance by the bytes it moves (the step is bandwidth-bound)
+    name = max(groups, key=lambda k: sum(c.bytes for c in groups[k]))
+    return name, groups[name]
 
 
 def algorithmic_bytes(M, K, N, tilecoo_bytes):
@@ -62,20 +81,112 @@ def kernel_source_digest():
     return h.hexdigest()
 
 
-def measured_traffic():
+def measured_traffic(kernel):
     """HBM bytes per dominant-kernel launch from the committed counter summary
     (FETCH_SIZE + WRITE_SIZE, each scaled by the copy-kernel calibration), or
-    None when the summary is missing or was taken on other kernel sources."""
+    None when the summary is missing, covers another kernel instance or was
+    taken on other kernel sources."""
     try:
         with open(TRAFFIC_PROFILE) as fh:
             for line in fh:
                 if line.startswith("traffic_json:"):
                     rec = json.loads(line.split(":", 1)[1])
-                    if rec.get("kernel_sources_sha256") == kernel_source_digest():
+                    if (rec.get("kernel_sources_sha256") == kernel_source_digest()
+                            and rec.get("kernel") == kernel):
                         return rec
     except OSError:
         pass
     return None
+
+
+def pmc_summary(fetch_csv, write_csv, sq_csv, log_path):
+    """Turn the rocprofv3 --pmc CSVs of a --pmc-pass run into the traffic
+    summary (markdown on stdout, ending in the traffic_json line bench.py
+    reads).  No GPU needed."""
+    import csv
+    meta = None
+    with open(log_path) as fh:
+        for line in fh:
+            if line.startswith('{"pmc_pass"'):
+                meta = json.loads(line)
+    if meta is None:
+        raise SystemExit(f"no pmc_pass line in {log_path}")
+    kernel = meta["kernel"]
+
+    def read(path):
+        rows = {}
+        for r in csv.DictReader(open(path)):
+            d = rows.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"]})
+            d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        return [rows[k] for k in sorted(rows)]
+
+    def is_dom(d):
+        return d["name"].replace("void fqk::", "").split("(")[0].strip() == kernel
+
+    def is_copy(d):
+        return "copyBuffer" in d["name"]
+
+    f, w = read(fetch_csv), read(write_csv)
+    fd = [d["FETCH_SIZE"] for d in f if is_dom(d)]
+    wd = [d["WRITE_SIZE"] for d in w if is_dom(d)]
+    fc = [d["FETCH_SIZE"] for d in f if is_copy(d)]
+    wc = [d["WRITE_SIZE"] for d in w if is_copy(d)]
+    if not fd or not fc or len(fd) != len(wd):
+        raise SystemExit("dominant kernel or copy kernel missing from the counter CSVs")
+    cal = meta["copy_bytes"]
+    ff, wf = cal / (fc[-1] * 1024), cal / (wc[-1] * 1024)
+    fetch = sum(fd) / len(fd) * 1024 * ff
+    write = sum(wd) / len(wd) * 1024 * wf
+    alg = meta["algorithmic_bytes_per_launch"]
+    cases = meta["pmc_pass"]
+    out = [f"Kernel `{kernel}`: launches {', '.join(cases)} of the Llama-3-8B decode step, "
+           f"each once per rotated weight copy ({meta['copies']} copies), then one plain device "
+           f"copy of {cal} bytes that calibrates the counters.", "",
+           "## Calibration", "",
+           f"The copy kernel moves {cal} bytes each way: FETCH_SIZE read {fc[-1]:.2f} KiB, "
+           f"WRITE_SIZE {wc[-1]:.2f} KiB, so the factors are fetch {ff:.4f} and write {wf:.4f}.",
+           "", "## Traffic per launch (calibrated)", "", "| case | FETCH MB | WRITE MB |",
+           "|---|---|---|"]
+    n = len(cases)
+    for i, c in enumerate(cases):
+        fs = [fd[j] for j in range(i, len(fd), n)]
+        ws_ = [wd[j] for j in range(i, len(wd), n)]
+        out.append(f"| {c} | {sum(fs) / len(fs) * 1024 * ff / 1e6:.2f} | "
+                   f"{sum(ws_) / len(ws_) * 1024 * wf / 1e6:.3f} |")
+    out += ["", f"Mean over the {len(fd)} launches: fetch {fetch / 1e6:.2f} MB + write "
+                f"{write / 1e6:.3f} MB = {(fetch + write) / 1e6:.2f} MB per launch, against "
+                f"{alg / 1e6:.2f} MB of algorithmic bytes per launch ({(fetch + write) / alg:.3f}x)."]
+    if sq_csv:
+        q = [d for d in read(sq_csv) if is_dom(d)]
+        tot = {}
+        for d in q:
+            for k, v in d.items():
+                if k != "name":
+                    tot[k] = tot.get(k, 0.0) + v
+        out += ["", "## SQ counters (sums over the same launches)", "", "| counter | value |",
+                "|---|---|"]
+        out += [f"| {k} | {v:.4g} |" for k, v in sorted(tot.items())]
+        wc_ = tot.get("SQ_WAVE_CYCLES", 0.0)
+        if wc_:
+            ratios = []
+            for k, lab in [("SQ_ACTIVE_INST_VALU", "VALU-active"), ("SQ_ACTIVE_INST_LDS", "LDS-active")]:
+                if k in tot:
+                    ratios.append(f"{lab} / wave cycles: {tot[k] / wc_:.3f}")
+            if "SQ_LDS_BANK_CONFLICT" in tot and tot.get("SQ_ACTIVE_INST_LDS"):
+                ratios.append("LDS bank-conflict cycles / LDS-active cycles: "
+                              f"{tot['SQ_LDS_BANK_CONFLICT'] / tot['SQ_ACTIVE_INST_LDS']:.3f}")
+            if "SQ_INSTS_VALU" in tot and tot.get("SQ_WAVES"):
+                ratios.append(f"VALU instructions per wave: {tot['SQ_INSTS_VALU'] / tot['SQ_WAVES']:.0f}")
+            out += ["", "; ".join(ratios) + "."]
+    rec = {"kernel": kernel, "kernel_sources_sha256": kernel_source_digest(),
+           "hbm_bytes_per_launch": round(fetch + write), "fetch_bytes_per_launch": round(fetch),
+           "write_bytes_per_launch": round(write), "algorithmic_bytes_per_launch": round(alg),
+           "fetch_factor": round(ff, 5), "write_factor": round(wf, 5), "launches": len(fd)}
+    out += ["", "bench.py reads the line below and reports `hbm_bytes_per_launch` as "
+                "roofline.traffic only while the kernel sources still hash to "
+                "`kernel_sources_sha256` and the dominant kernel is the same instance.", "",
+            "traffic_json: " + json.dumps(rec)]
+    print("\n".join(out))
 
 
 def cpu_baseline(tilecoo_bytes: dict, budget_s: float = 20.0):
@@ -217,7 +328,14 @@ def main():
                     help="no timing: eager launches of the dominant kernel's matmuls over the "
                          "rotated copies, then a plain copy of COPY_CAL_BYTES, for rocprofv3 "
                          "--pmc FETCH_SIZE / WRITE_SIZE collection")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "SQ_CSV", "LOG"),
+                    help="no GPU: summarise the rocprofv3 counter CSVs of --pmc-pass runs "
+                         "(SQ_CSV may be '-') into the traffic profile text")
     args = ap.parse_args()
+    if args.pmc_summary:
+        fcsv, wcsv, sqcsv, logp = args.pmc_summary
+        pmc_summary(fcsv, wcsv, None if sqcsv == "-" else sqcsv, logp)
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -289,7 +407,7 @@ def main():
     if args.pmc_pass:
         # Each dominant-kernel matmul once per weight copy, then the copy
         # kernel whose byte count calibrates the counters.
-        dom = [c for c in order if c.M >= DOMINANT_MIN_M]
+        dom_name, dom = dominant_kernel(fq, order)
         for r in range(R):
             for c in dom:
                 launch(c, r, "fused")
@@ -298,7 +416,8 @@ def main():
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
-        print(json.dumps({"pmc_pass": [f"{c.name}/M{c.M}" for c in dom], "copies": R,
+        print(json.dumps({"pmc_pass": [f"{c.name}/M{c.M}" for c in dom], "kernel": dom_name,
+                          "copies": R,
                           "algorithmic_bytes_per_launch": sum(c.bytes for c in dom) / len(dom),
                           "copy_bytes": COPY_CAL_BYTES}), flush=True)
         return
@@ -359,6 +478,7 @@ def main():
         us = per_launch_us(c, "fused", reps)
         fused_total_us += us
         d = {"shape": c.name, "M": c.M, "K": c.K, "N": c.N, "bytes": c.bytes,
+             "kernel": kernel_name(fq, c.M, c.K, c.N),
              "fused_us": round(us, 3), "fused_GBs": round(c.bytes / us / 1e3, 1),
              "pct_peak": round(100 * c.bytes / us / 1e3 / HBM_PEAK_GBS, 1)}
         if not args.no_compare:
@@ -393,16 +513,20 @@ def main():
             del Ws
             torch.cuda.empty_cache()
 
-    # Dominant kernel: the fused kernel with the MFMA sparse mapping (the step's
-    # M = 4, 8, 16 matmuls), which takes most of the step; the M = 1 matmuls
-    # (gather mapping) are reported beside it.
+    # Dominant kernel: the fused kernel instance that moves most of the
+    # step's bytes (64-column strips with the MFMA outlier mapping: gate+up
+    # and down at M = 4, 8, 16); the other launches are reported beside it.
+    dom_name, dom_cases = dominant_kernel(fq, order)
+    dom_keys = {(c.name, c.M) for c in dom_cases}
+
     def agg(sel):
         b = sum(d["bytes"] for d in details if sel(d))
         t = sum(d["fused_us"] for d in details if sel(d))
-        return b, t
-    dom_b, dom_t = agg(lambda d: d["M"] >= DOMINANT_MIN_M)
-    gat_b, gat_t = agg(lambda d: d["M"] < DOMINANT_MIN_M)
-    traffic_rec = measured_traffic()
+        n = sum(1 for d in details if sel(d))
+        return b, t, n
+    dom_b, dom_t, dom_n = agg(lambda d: (d["shape"], d["M"]) in dom_keys)
+    oth_b, oth_t, _ = agg(lambda d: (d["shape"], d["M"]) not in dom_keys)
+    traffic_rec = measured_traffic(dom_name)
     achieved = dom_b / (dom_t * 1e-6) / 1e9
     result = {
         "metric": METRIC,
@@ -429,17 +553,16 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "matmul_kernel<1, 1, true, true, NW> (fused, MFMA sparse mapping, M=4,8,16)",
+            "kernel": dom_name,
+            "launches": sorted(f"{n}/M{m}" for n, m in dom_keys),
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": (traffic_rec or {}).get("hbm_bytes_per_launch"),
-            "bytes_per_launch": round(dom_b / max(1, sum(1 for d in details
-                                                         if d["M"] >= DOMINANT_MIN_M))),
-            "us_per_launch": round(dom_t / max(1, sum(1 for d in details
-                                                      if d["M"] >= DOMINANT_MIN_M)), 3),
-            "gather_mapping_GBs": round(gat_b / (gat_t * 1e-6) / 1e9, 1) if gat_t else None,
+            "bytes_per_launch": round(dom_b / max(1, dom_n)),
+            "us_per_launch": round(dom_t / max(1, dom_n), 3),
+            "other_launches_GBs": round(oth_b / (oth_t * 1e-6) / 1e9, 1) if oth_t else None,
         },
         "per_matmul": details,
         "pack_s": {k: round(v, 3) for k, v in pack_s.items()},

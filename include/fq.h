@@ -288,6 +288,19 @@ enum { FQ_SPARSE_WAVES = 64 };
 fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes);
 
 /*
+ * fq_launch_config -- the launch the fused entry point would make for pr
+ * (for tools and benchmarks; nothing is launched).  Outputs (host):
+ *   cfg[0] strip width in columns (32 or 64)   cfg[1] K ranges per strip (split)
+ *   cfg[2] dense waves per workgroup           cfg[3] outlier-only waves per workgroup
+ *   cfg[4] outlier mapping (FQ_SPARSE_GATHER or FQ_SPARSE_MFMA)
+ *   cfg[5] workgroups in the grid              cfg[6] 1 under Stream-K, else 0
+ *   cfg[7] dynamic LDS bytes per workgroup
+ * buckets_per_tile is the Tile-COO's (1..256).
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_UNSUPPORTED.
+ */
+fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t cfg[8]);
+
+/*
  * fq_w4a16_outlier_matmul -- fused Y = X dequant(W_Q) + X W_O in one kernel
  * (the paper's sparse-dense fused operator, Sec. 3.1 and Sec. 4).  Dense and
  * sparse work for the same 128 x 64 tile run in the same workgroup and read

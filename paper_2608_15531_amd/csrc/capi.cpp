@@ -116,6 +116,27 @@ const char* fq_status_string(fq_status s) {
   return "unknown status";
 }
 
+fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t cfg[8]) {
+  if (!cfg) return FQ_ERR_NULL;
+  fq_status st = check_problem(pr);
+  if (st != FQ_OK) return st;
+  const int mapping = pr->flags & FQ_SPARSE_MASK;
+  const int mode = mapping == FQ_SPARSE_GATHER ? 0 : mapping == FQ_SPARSE_MFMA ? 1 : -1;
+  fqi::Plan pl;
+  if (!fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, true, true, buckets_per_tile, 0, &pl, mode,
+                      plan_opts(pr)))
+    return FQ_ERR_UNSUPPORTED;
+  cfg[0] = 16 * pl.NCB;
+  cfg[1] = pl.S;
+  cfg[2] = pl.NW;
+  cfg[3] = pl.NWS;
+  cfg[4] = pl.MODE == 0 ? FQ_SPARSE_GATHER : FQ_SPARSE_MFMA;
+  cfg[5] = pl.G * pl.n_slabs;
+  cfg[6] = pl.stream;
+  cfg[7] = int32_t(pl.lds_bytes);
+  return FQ_OK;
+}
+
 fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes) {
   if (!bytes) return FQ_ERR_NULL;
   fq_status st = check_problem(pr);

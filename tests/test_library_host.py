@@ -324,3 +324,36 @@ def test_debug_decode_rejects(lib):
     assert lib.fq_debug_decode_tile_coo(None, 256, 128, FAKE, FAKE, FAKE, None) == 1
     assert lib.fq_debug_decode_tile_coo(C.byref(tc), 250, 128, FAKE, FAKE, FAKE, None) == 2
     assert lib.fq_debug_decode_tile_coo(C.byref(tc), 256, 128, None, FAKE, FAKE, None) == 1
+
+
+# ----------------------------------------------------- launch configuration --
+
+@pytest.mark.parametrize("M,K,N,expect", [
+    # wide matrices: 64-column strips, no split; the gather mapping at M = 1
+    (1, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="gather")),
+    (16, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="mfma")),
+    # narrow, K <= 8192: 32-column strips without split-K
+    (1, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, mapping="mfma")),
+    (8, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8)),
+    # few strips and 12+ rows: split 2, four waves
+    (16, 4096, 4096, dict(strip_cols=32, split_k=2, dense_waves=4)),
+    # long K: 64-column strips split to about 512 workgroups
+    (4, 14336, 4096, dict(strip_cols=64, split_k=8, dense_waves=4, workgroups=512)),
+])
+def test_launch_config_defaults(lib, M, K, N, expect):
+    cfg = fq.fq_launch_config(M, K, N)
+    for k, v in expect.items():
+        assert cfg[k] == v, (k, cfg)
+    assert cfg["outlier_waves"] == 0 and not cfg["stream_k"]
+    assert cfg["lds_bytes"] <= 160 * 1024
+
+
+def test_launch_config_switches(lib):
+    assert fq.fq_launch_config(4, 4096, 4096, flags=fq.FQ_STRIP_64)["strip_cols"] == 64
+    assert fq.fq_launch_config(4, 4096, 28672, flags=fq.FQ_STRIP_32)["strip_cols"] == 32
+    ew = fq.fq_launch_config(4, 4096, 28672, flags=fq.FQ_SPARSE_WAVES)
+    assert ew["outlier_waves"] == ew["dense_waves"] // 2
+    assert fq.fq_launch_config(4, 4096, 28672, flags=fq.FQ_SCHED_STREAM_K)["stream_k"]
+    assert fq.fq_launch_config(4, 4096, 4096, split_k=3)["split_k"] == 3
+    with pytest.raises(fq.FqError):
+        fq.fq_launch_config(5, 4096, 4096, sparse="gather")
