@@ -295,6 +295,121 @@ def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
                       "speedup": geo, "per_matmul_us": table}), flush=True)
 
 
+MFMA_PEAK_TFLOPS = 2500.0   # MI355X dense bf16
+
+
+def unfused_workspace_bytes(fq, M, K, N):
+    """Workspace that serves the fused, unfused and dense-only entry points."""
+    pr = fq._problem(M, K, N, 0, 0)
+    need = fq.C.c_size_t(0)
+    fq.load().fq_workspace_bytes_unfused(fq.C.byref(pr), fq.C.byref(need))
+    return max(need.value, fq.fq_workspace_bytes(M, K, N))
+
+
+def mfma_flops(fq, M, K, N):
+    """FLOPs the matrix cores execute in one fused launch: per 16-row block and
+    128 x (strip width) tile, 4 x NCB dense MFMAs, 4 row-sum MFMAs and, with
+    the MFMA outlier mapping, 4 x NCB image MFMAs of 16 x 16 x 32."""
+    c = fq.fq_launch_config(M, K, N)
+    ncb = c["strip_cols"] // 16
+    slabs = (M + 31) // 32
+    mb = 1 if min(M, 32) <= 16 else 2
+    per_tile = 4 * ncb + 4 + (4 * ncb if c["mapping"] == "mfma" else 0)
+    return slabs * mb * (N // c["strip_cols"]) * (K // 128) * per_tile * 16 * 16 * 32 * 2
+
+
+def sweep(fq, torch, which, dev, copies_min=4):
+    """Per-matmul timings of the other workloads (not the step): the density
+    and structure sweep, the Llama-3-70B decode layer, and the larger-M
+    crossover with MFMA utilisation.  One JSON line per matmul."""
+    from synth import make_activations, make_problem, seed_for
+    if which == "density":
+        cases = [(2, 0, 8, 4096, 14336, f, d) for d in ("uniform", "clustered")
+                 for f in (0.0, 0.005, 0.01, 0.02, 0.05)]
+    elif which == "70b":
+        shapes = [("qkv70", 8192, 10240), ("o70", 8192, 8192), ("gate_up70", 8192, 57344),
+                  ("down70", 28672, 8192)]
+        cases = [(3, si, M, K, N, 0.01, "uniform") for si, (_, K, N) in enumerate(shapes)
+                 for M in (1, 8, 16, 32)]
+    else:
+        cases = [(4, si, M, K, N, 0.01, "uniform")
+                 for si, (K, N) in enumerate([(4096, 14336), (14336, 4096)])
+                 for M in (32, 64, 128)]
+
+    def capture(fn):
+        g = torch.cuda.CUDAGraph()
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            fn()
+        torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            fn()
+        torch.cuda.synchronize()
+        return g
+
+    def per_launch_us(fn, L, reps=4):
+        g = capture(lambda: [fn(i) for i in range(L)])
+        g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * L)
+
+    # weights per (shape, density, structure): enough rotated copies to pass 1 GiB
+    weights = {}
+    for cfg, si, M, K, N, frac, dist in cases:
+        key = (K, N, frac, dist)
+        if key in weights:
+            continue
+        weights.clear()
+        torch.cuda.empty_cache()
+        p = make_problem(1, K, N, frac=frac, dist=dist, seed=seed_for(cfg, si, 0) + int(frac * 1000))
+        host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v)
+        R = max(copies_min, -(-(1 << 30) // (K * N // 2 + host.sizes.bytes)))
+        weights[key] = ([fq.to_device(p, dev)[1:] for _ in range(R)],
+                        [fq.TileCOODevice(host, dev) for _ in range(R)], host, p.meta)
+        W, T, host, meta = weights[key]
+        mis = {1: 0, 8: 1, 16: 2, 32: 3, 64: 1, 128: 2}
+        for c2 in [c for c in cases if (c[3], c[4], c[5], c[6]) == key]:
+            M2 = c2[2]
+            xb = make_activations(M2, K, seed_for(cfg, si, mis.get(M2, 0)))
+            x = torch.from_numpy(xb.view(np.int16).copy()).view(torch.bfloat16).to(dev)
+            Y = torch.empty((M2, N), dtype=torch.bfloat16, device=dev)
+            ws = torch.zeros(unfused_workspace_bytes(fq, M2, K, N), dtype=torch.uint8, device=dev)
+            L = 4 * len(W)
+            us = per_launch_us(lambda i: fq.fq_w4a16_outlier_matmul(
+                x, *W[i % len(W)], T[i % len(W)], Y=Y, ws=ws), L)
+            us_unf = per_launch_us(lambda i: fq.fq_w4a16_outlier_matmul_unfused(
+                x, *W[i % len(W)], T[i % len(W)], Y=Y, ws=ws), L)
+            us_dense = per_launch_us(lambda i: fq.fq_w4a16_matmul(
+                x, *W[i % len(W)], Y=Y, ws=ws), L)
+            nbytes = algorithmic_bytes(M2, K, N, int(host.sizes.bytes))
+            nnz = int(host.sizes.nnz)
+            rec = {"sweep": which, "K": K, "N": N, "M": M2, "frac": frac, "dist": dist,
+                   "nnz": nnz, "tilecoo_bytes": int(host.sizes.bytes), "bytes": nbytes,
+                   "kernel": kernel_name(fq, M2, K, N), "copies": len(W),
+                   "fused_us": round(us, 3), "fused_GBs": round(nbytes / us / 1e3, 1),
+                   "pct_hbm_peak": round(100 * nbytes / us / 1e3 / HBM_PEAK_GBS, 1),
+                   "unfused_us": round(us_unf, 3), "dense_only_us": round(us_dense, 3),
+                   "fused_vs_unfused": round(us_unf / us, 3)}
+            if "realised_share" in meta:
+                rec["clustered_share"] = round(meta["realised_share"], 3)
+            if which == "large-m":
+                alg = 2 * M2 * K * N + 2 * M2 * nnz
+                mf = mfma_flops(fq, M2, K, N)
+                rec.update(alg_TFLOPs=round(alg / us / 1e6, 1),
+                           mfma_TFLOPs=round(mf / us / 1e6, 1),
+                           mfma_util_pct=round(100 * mf / us / 1e6 / MFMA_PEAK_TFLOPS, 2))
+            print(json.dumps(rec), flush=True)
+
+
 class Case:
     """One (shape, M) matmul with R rotated weight copies on the device."""
 
@@ -328,6 +443,10 @@ def main():
                     help="no timing: eager launches of the dominant kernel's matmuls over the "
                          "rotated copies, then a plain copy of COPY_CAL_BYTES, for rocprofv3 "
                          "--pmc FETCH_SIZE / WRITE_SIZE collection")
+    ap.add_argument("--sweep", choices=["density", "70b", "large-m"],
+                    help="no step timing: per-matmul timings of the density / structure "
+                         "sweep (M=8, 4096x14336), the Llama-3-70B decode linears (M=1..32) "
+                         "or the larger-M crossover (M=32..128, with MFMA utilisation)")
     ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "SQ_CSV", "LOG"),
                     help="no GPU: summarise the rocprofv3 counter CSVs of --pmc-pass runs "
                          "(SQ_CSV may be '-') into the traffic profile text")
@@ -351,6 +470,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     R = args.copies
+    if args.sweep:
+        sweep(fq, torch, args.sweep, dev)
+        return
 
     # ---------------------------------------------------------- inputs
     cases = []
@@ -378,12 +500,7 @@ def main():
     step_bytes = sum(c.bytes for c in order)
 
     max_ws = max(fq.fq_workspace_bytes(c.M, c.K, c.N) for c in cases)
-    max_ws_unf = 0
-    for c in cases:
-        pr = fq._problem(c.M, c.K, c.N, 0, 0)
-        need = fq.C.c_size_t(0)
-        fq.load().fq_workspace_bytes_unfused(fq.C.byref(pr), fq.C.byref(need))
-        max_ws_unf = max(max_ws_unf, need.value)
+    max_ws_unf = max(unfused_workspace_bytes(fq, c.M, c.K, c.N) for c in cases)
     ws = torch.zeros(max(max_ws, max_ws_unf), dtype=torch.uint8, device=dev)
 
     def launch(c, r, variant):
