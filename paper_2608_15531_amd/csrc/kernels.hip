@@ -943,29 +943,37 @@ int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
 }
 
 // The launch shape (strip width, split, waves per workgroup) the library
-// picks when the caller forces none.  Measured on MI355X over the Llama-3-8B
-// decode linears at M = 1..16 (graph replay, rotated weights):
-//  * N / 64 strips fill the GPU (gate+up): 64-column strips, no split.
-//  * Narrow N, K <= 8192 (qkv, o): 32-column strips (128-byte segments of
-//    each packed row, which stream as well as 256-byte ones) and no split,
-//    eight waves -- a cross-workgroup split-K reduction costs three
-//    dependent trips through the device-coherent memory level (about 2 us),
-//    more than the extra instructions per byte of the narrower strip.  With
-//    fewer than 192 strips and 12 or more rows the per-tile work is heavy
-//    enough that covering all CUs pays: split 2, four waves.
-//  * Narrow N, long K (down): 64-column strips split until there are about
-//    512 workgroups, four waves each.
+// picks when the caller forces none.  Measured on MI355X (graph replay,
+// rotated weights) over the Llama-3-8B and -70B decode linears and the
+// 4096 x 14336 density-sweep shape at M = 1..16:
+//  * 160 or more 64-column strips (gate+up, 4096 x 14336, 70B qkv and
+//    gate+up): 64-column strips and the split-K default below (no split
+//    once the strips fill the CUs).
+//  * Fewer strips, K <= 8192 (8B qkv and o, 70B o): 32-column strips
+//    (128-byte segments of each packed row, which stream as well as
+//    256-byte ones), no split, eight waves -- a cross-workgroup split-K
+//    reduction costs three dependent trips through the device-coherent
+//    memory level (about 2 us), more than the extra instructions per byte of
+//    the narrower strip.  With 12 or more rows the per-tile work is heavier
+//    and covering every CU pays, unless the 32-column strips already give
+//    192 workgroups of at most 32 tiles: 64-column strips split to at least
+//    256 workgroups, four waves.
+//  * Long K (down): 64-column strips split to about 512 workgroups, four
+//    waves.
 struct Shape {
   int ncb, split, waves;   // split 0: the split-K default for that width
 };
 Shape default_shape(int T, int N, int n_slabs, int slab_M) {
   const int64_t units64 = int64_t(N / 64) * n_slabs, units32 = int64_t(N / 32) * n_slabs;
-  if (units64 >= 256) return {4, 0, 0};
+  if (units64 >= 160) return {4, 0, 0};
+  int S = 1;
   if (T <= 64) {
-    if (units32 < 192 && slab_M >= 12 && T >= 16) return {2, 2, 4};
+    if (slab_M >= 12 && (units32 < 192 || T > 32)) {
+      while (units64 * S < 256 && 2 * S <= T / 8) S *= 2;
+      return {4, S, 4};
+    }
     return {2, 1, T >= 8 ? 8 : 4};
   }
-  int S = 1;
   while (units64 * S < 512 && 2 * S <= T / 8) S *= 2;
   return {4, S, 4};
 }

@@ -335,8 +335,13 @@ def test_debug_decode_rejects(lib):
     # narrow, K <= 8192: 32-column strips without split-K
     (1, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, mapping="mfma")),
     (8, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8)),
-    # few strips and 12+ rows: split 2, four waves
-    (16, 4096, 4096, dict(strip_cols=32, split_k=2, dense_waves=4)),
+    # few strips and 12+ rows: 64-column strips split to 256 workgroups, four waves
+    (16, 4096, 4096, dict(strip_cols=64, split_k=4, dense_waves=4, workgroups=256)),
+    # 32-column strips already give 192 workgroups of 32 tiles: no split
+    (16, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8)),
+    # 160+ 64-column strips: 64-column strips, no split, eight waves
+    (8, 4096, 14336, dict(strip_cols=64, split_k=1, dense_waves=8)),
+    (1, 8192, 10240, dict(strip_cols=64, mapping="gather")),
     # long K: 64-column strips split to about 512 workgroups
     (4, 14336, 4096, dict(strip_cols=64, split_k=8, dense_waves=4, workgroups=512)),
 ])
