@@ -47,8 +47,9 @@ def kernel_name(fq, M, K, N):
     mb = 1 if min(M, 32) <= 16 else 2
     mode = 0 if c["mapping"] == "gather" else 1
     sk = "true" if c["stream_k"] else "false"
+    xs = "true" if c["x_staged"] else "false"
     return (f"matmul_kernel<{mb}, {mode}, {c['strip_cols'] // 16}, true, true, "
-            f"{c['dense_waves']}, {sk}, {c['outlier_waves']}>")
+            f"{c['dense_waves']}, {sk}, {c['outlier_waves']}, {xs}>")
 
 
 def dominant_kernel(fq, cases):

@@ -295,10 +295,12 @@ fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes);
  *   cfg[4] outlier mapping (FQ_SPARSE_GATHER or FQ_SPARSE_MFMA)
  *   cfg[5] workgroups in the grid              cfg[6] 1 under Stream-K, else 0
  *   cfg[7] dynamic LDS bytes per workgroup
+ *   cfg[8] 1 when each tile's X slice is loaded row by row and reordered into
+ *          MFMA operand order through LDS (MFMA mapping at 9..16 rows), else 0
  * buckets_per_tile is the Tile-COO's (1..256).
  * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_UNSUPPORTED.
  */
-fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t cfg[8]);
+fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t cfg[9]);
 
 /*
  * fq_w4a16_outlier_matmul -- fused Y = X dequant(W_Q) + X W_O in one kernel

@@ -116,7 +116,7 @@ const char* fq_status_string(fq_status s) {
   return "unknown status";
 }
 
-fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t cfg[8]) {
+fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t cfg[9]) {
   if (!cfg) return FQ_ERR_NULL;
   fq_status st = check_problem(pr);
   if (st != FQ_OK) return st;
@@ -134,6 +134,7 @@ fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32
   cfg[5] = pl.G * pl.n_slabs;
   cfg[6] = pl.stream;
   cfg[7] = int32_t(pl.lds_bytes);
+  cfg[8] = pl.XS;
   return FQ_OK;
 }
 

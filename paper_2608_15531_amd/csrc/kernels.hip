@@ -53,7 +53,7 @@
 
 namespace fqk {
 
-constexpr int XS = fqi::kXStride;   // LDS row stride of a staged X slice, elements
+constexpr int kXRow = fqi::kXStride;   // LDS row stride of a staged X slice, elements
 constexpr int kGatherLimitM = fqi::kGatherLimitM;
 
 // Kernel arguments.  The first 64 bytes (one scalar-cache line) hold what
@@ -78,6 +78,7 @@ struct MatmulArgs {
   int off_shc;         // per-wave sparse output buffers (gather mode)
   int off_flag;
   int off_trash;       // 16 bytes that padding slots are written to (MFMA mode)
+  int off_xs;          // per-wave X stages (MFMA mode, one 16-row block)
   const float* y_addend;
   void* Y;
   float* partials;
@@ -143,16 +144,27 @@ struct Operands {
   uint32_t lw;       // Wq: row h of a 16-row step block, columns n0 + NCB*c4 .. + NCB-1
   uint32_t ls;       // scales of those columns
   uint32_t lz;       // zero-point word holding them
-  uint32_t lx[MB];   // X: MODE 0 chunk lane; MODE 1 row 16mb + c4, elements 8h..
+  uint32_t lx[4 * MB];   // X: MODE 0 chunk lane; MODE 1 see load_tile_dense
 };
 
+// X staging (template flag XSTAGE; MFMA mapping, one 16-row block, chosen from
+// 9 rows on): the tile's X slice is loaded row by row -- each load covers
+// 4 rows x 256 bytes, 8 whole cache lines, where loads in operand order touch
+// 16 half lines -- and reordered into operand order through a 4 KB stage in
+// LDS.  With fewer rows the operand-order loads touch few lines and the stage
+// only adds latency.
+
 // The loads of a tile that do not depend on the Tile-COO offsets: packed
-// codes, scales and zero-points (dense path) and the tile's slice of X.
+// codes, scales and zero-points (dense path) and the tile's slice of X:
+// MODE 0 one chunk per lane; MODE 1 four loads per 16-row block at offsets
+// set up once per wave (staged: load j = row 4j + h, elements 8 c4 .. + 7;
+// else the A fragments [mb][step], row 16 mb + c4, elements 32 step + 8 h
+// .. + 7).
 // Every load is unconditional (offsets clamped into range) so the compiler
 // counts outstanding loads exactly across the prefetch.  A wave-wide load of
 // one step covers 4 packed rows x (16 NCB) columns: 128-byte row segments for
 // 32-column strips, 256-byte ones for 64-column strips.
-template <int MB, int MODE, int NCB, bool DENSE>
+template <int MB, int MODE, int NCB, bool DENSE, bool XSTAGE>
 __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Operands<MB>& op,
                                                 int t, int n0, TileRegs<MB, MODE, NCB>& r) {
   if (DENSE) {
@@ -173,6 +185,9 @@ __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Opera
   const uint32_t xt = uint32_t(t) * 256u;
   if (MODE == 0) {
     r.x[0] = buf_load16(op.x, op.lx[0], xt);
+  } else if (XSTAGE) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r.x[j] = buf_load16(op.x, op.lx[j], xt);
   } else {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
@@ -247,7 +262,7 @@ __device__ __forceinline__ void gather_x(const MatmulArgs& a, const uint16_t* xs
 #pragma unroll
   for (int m = 0; m < kGatherLimitM; ++m) {
     if (m < a.M) {
-      const uint16_t* xr = xs + m * XS;
+      const uint16_t* xr = xs + m * kXRow;
       g.x01[m] = __builtin_amdgcn_perm(uint32_t(xr[p1]), uint32_t(xr[p0]), 0x05040100u);
       g.x23[m] = __builtin_amdgcn_perm(uint32_t(xr[p3]), uint32_t(xr[p2]), 0x05040100u);
     }
@@ -276,7 +291,7 @@ __device__ __forceinline__ void sparse_gather(const MatmulArgs& a, const uint16_
   }
   const uint32_t p4 = chunk_pos4(d.rows & 0x7F7F7F7Fu);
   for (int m = 0; m < a.M; ++m) {
-    const uint16_t* xr = xs + m * XS;
+    const uint16_t* xr = xs + m * kXRow;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t v = slot_val(d, j);
@@ -363,9 +378,10 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
   for (int j = 0; j < 4; ++j) lds_store16(addr[j], 0u);
 }
 
-template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS>
+template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS, bool XSTAGE>
 __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args) {
   static_assert(NCB == 4 || (NCB == 2 && MODE == 1), "32-column strips use the MFMA outlier mapping");
+  static_assert(!XSTAGE || (MODE == 1 && MB == 1), "X staging: MFMA mapping, one 16-row block");
   // NWS > 0: warp specialisation (Sec. 3.1) -- NW dense waves and NWS outlier
   // waves share the strip's K range and the output reduction.
   constexpr int NT = NW + NWS;                 // waves per workgroup
@@ -459,13 +475,21 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
   if (MODE == 0) {
     // rows past M load row M-1 (the slice store below is then a rewrite)
     op.lx[0] = (uint32_t(min(lane >> 4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(lane & 15)) * 2u;
+  } else if (XSTAGE) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)   // rows past M load row M-1, never stored
+      op.lx[j] = (uint32_t(min(4 * j + h, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(c4)) * 2u;
   } else {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)   // rows past M load row M-1, never stored
       op.lx[mb] = (uint32_t(min(mb * 16 + c4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(h)) * 2u;
   }
   const uint32_t img = lds_address(bo);                  // this wave's image
-  const uint32_t trash = lds_address(smem + a.off_trash);
+  // X stage of this wave (16 rows x 256 bytes, 16-byte chunk q of row r at
+  // position q ^ r); its first 16 bytes double as the trash word, written by
+  // the scatter only between the stage's read and its next write
+  unsigned char* xst = smem + a.off_xs + size_t(wave) * 4096;
+  const uint32_t trash = lds_address(XSTAGE ? xst : smem + a.off_trash);
 
 
   // The current segment (read by the lambdas below).
@@ -490,7 +514,7 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
       load_tile_sparse<MB, MODE, NCB, SPARSE>(op, lane, g0, g1, r);
     };
     auto issue = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
-      load_tile_dense<MB, MODE, NCB, DENSE>(a, op, t, n0, r);
+      load_tile_dense<MB, MODE, NCB, DENSE, XSTAGE>(a, op, t, n0, r);
       issue_sparse(t, r);
     };
 
@@ -502,11 +526,23 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
         // same values, which keeps the store unconditional), then read it back
         // in MFMA operand order
         const int m = min(lane >> 4, a.M - 1);
-        *reinterpret_cast<uint4*>(xs + m * XS + 8 * (lane & 15)) = permute_chunk(cur.x[0]);
+        *reinterpret_cast<uint4*>(xs + m * kXRow + 8 * (lane & 15)) = permute_chunk(cur.x[0]);
         __builtin_amdgcn_wave_barrier();
   #pragma unroll
         for (int step = 0; step < 4; ++step)
-          A[0][step] = *reinterpret_cast<const bf16x8_t*>(xs + min(c4, a.M - 1) * XS + step * 32 + 8 * h);
+          A[0][step] = *reinterpret_cast<const bf16x8_t*>(xs + min(c4, a.M - 1) * kXRow + step * 32 + 8 * h);
+      } else if (XSTAGE) {
+        // load j of lane (c4, h) holds chunk c4 of row 4j + h; fragment
+        // `step` of lane (c4, h) is chunk 4 step + h of row c4.  Both
+        // directions touch 16 distinct 16-byte bank groups per 16 lanes.
+  #pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<uint4*>(xst + (4 * j + h) * 256 + ((c4 ^ (4 * j + h)) << 4)) = cur.x[j];
+        __builtin_amdgcn_wave_barrier();
+  #pragma unroll
+        for (int step = 0; step < 4; ++step)
+          A[0][step] = __builtin_bit_cast(bf16x8_t, permute_chunk(*reinterpret_cast<const uint4*>(
+                                                        xst + c4 * 256 + (((4 * step + h) ^ c4) << 4))));
       } else {
   #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
@@ -864,9 +900,9 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
   }
 }
 
-template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK, int NWS = 0>
+template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK, int NWS, bool XSTAGE>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS>;
+  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XSTAGE>;
   if (pl.lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -878,14 +914,23 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
   return int(hipGetLastError());
 }
 
+template <int MB, int MODE, int NCB, int NW, bool SK, bool XSTAGE>
+int launch_roles(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
+  if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8)) {
+    if (dense && sparse && pl.NWS > 0)
+      return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2, XSTAGE>(pl, a, s);
+  }
+  if (dense && sparse) return launch_variant<MB, MODE, NCB, true, true, NW, SK, 0, XSTAGE>(pl, a, s);
+  if (dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK, 0, XSTAGE>(pl, a, s);
+  return launch_variant<MB, MODE, NCB, false, true, NW, SK, 0, XSTAGE>(pl, a, s);
+}
+
 template <int MB, int MODE, int NCB, int NW, bool SK>
 int launch_sched(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
-  if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8)) {
-    if (dense && sparse && pl.NWS > 0) return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2>(pl, a, s);
+  if constexpr (MODE == 1 && MB == 1) {
+    if (pl.XS) return launch_roles<MB, MODE, NCB, NW, SK, true>(pl, a, dense, sparse, s);
   }
-  if (dense && sparse) return launch_variant<MB, MODE, NCB, true, true, NW, SK>(pl, a, s);
-  if (dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK>(pl, a, s);
-  return launch_variant<MB, MODE, NCB, false, true, NW, SK>(pl, a, s);
+  return launch_roles<MB, MODE, NCB, NW, SK, false>(pl, a, dense, sparse, s);
 }
 
 // Stream-K is built for 64-column strips only (the plan never combines it
@@ -1085,11 +1130,31 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   // reduction buffer (one tile per wave) reuses them
   const int n_slots = p.NWS > 0 ? p.NWS : p.NW;
   const size_t red_bytes = size_t(p.NW + p.NWS) * p.slab_M * (16 * p.NCB) * 4;
-  p.off_shc = align_up(std::max(n_slots * p.slot_bytes, red_bytes), 16);
-  const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * p.slab_M * kTileN * 4 : 0;
-  p.off_flag = align_up(p.off_shc + shc_bytes, 16);
-  p.off_trash = p.off_flag + 16;
-  p.lds_bytes = p.off_trash + 16;
+  p.XS = p.MODE == 1 && p.MB == 1 && p.slab_M >= kXStageMinM;
+  if (p.XS) {
+    // images, then a 4 KB X stage per wave.  After the tile loop the
+    // reduction buffer reuses them, and the split-K flag sits at the head of
+    // wave 0's stage when the reduction buffer ends before it.  Each wave's
+    // trash word is the head of its own stage.
+    p.off_xs = n_slots * p.slot_bytes;
+    const size_t end = std::max(p.off_xs + size_t(p.NW + p.NWS) * 4096, red_bytes);
+    p.off_shc = end;
+    p.off_trash = p.off_xs;
+    if (red_bytes <= p.off_xs) {
+      p.off_flag = p.off_xs;
+      p.lds_bytes = end;
+    } else {
+      p.off_flag = align_up(end, 16);
+      p.lds_bytes = p.off_flag + 16;
+    }
+  } else {
+    p.off_shc = align_up(std::max(n_slots * p.slot_bytes, red_bytes), 16);
+    const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * p.slab_M * kTileN * 4 : 0;
+    p.off_flag = align_up(p.off_shc + shc_bytes, 16);
+    p.off_trash = p.off_flag + 16;
+    p.off_xs = p.off_trash;   // no X stages
+    p.lds_bytes = p.off_trash + 16;
+  }
   if (p.lds_bytes > 160 * 1024) return false;
 
   // partial sums: [slab][strip][slot][row][strip width] fp32, every slab kSlabM rows apart
@@ -1130,6 +1195,7 @@ int launch_matmul(const Plan& pl, const MatmulPtrs& p, bool dense, bool sparse, 
   a.off_shc = int(pl.off_shc);
   a.off_flag = int(pl.off_flag);
   a.off_trash = int(pl.off_trash);
+  a.off_xs = int(pl.off_xs);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (sparse && p.n_groups == 0) {
     // No outliers: the fused launch drops its sparse half; a sparse-only

@@ -123,6 +123,8 @@ EXACT_CASES = [
     (8, 128, 64, 0.5, 0, c_params()),
     (2, 256, 64, 1.0, 0, c_params(buckets_per_tile=4)),
     (4, 512, 128, 0.0, 0, c_params()),
+    # nine rows: the smallest M whose X slice goes through the LDS stage
+    (9, 1152, 448, 0.03, 0, c_params()),
     # more than 32 rows: 32-row slabs in the grid, ragged last slab, split-K
     (33, 1024, 256, 0.02, 0, c_params()),
     (64, 2048, 512, 0.01, 3, c_params()),

@@ -331,17 +331,20 @@ def test_debug_decode_rejects(lib):
 @pytest.mark.parametrize("M,K,N,expect", [
     # wide matrices: 64-column strips, no split; the gather mapping at M = 1
     (1, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="gather")),
-    (16, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="mfma")),
+    (16, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="mfma", x_staged=True)),
     # narrow, K <= 8192: 32-column strips without split-K
     (1, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, mapping="mfma")),
-    (8, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8)),
+    (8, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_staged=False)),
     # few strips and 12+ rows: 64-column strips split to 256 workgroups, four waves
     (16, 4096, 4096, dict(strip_cols=64, split_k=4, dense_waves=4, workgroups=256)),
     # 32-column strips already give 192 workgroups of 32 tiles: no split
-    (16, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8)),
+    (16, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_staged=True)),
+    # X slices through the LDS stage from 9 rows to one 16-row block
+    (9, 4096, 6144, dict(x_staged=True)),
+    (17, 4096, 6144, dict(x_staged=False)),
     # 160+ 64-column strips: 64-column strips, no split, eight waves
     (8, 4096, 14336, dict(strip_cols=64, split_k=1, dense_waves=8)),
-    (1, 8192, 10240, dict(strip_cols=64, mapping="gather")),
+    (1, 8192, 10240, dict(strip_cols=64, mapping="gather", x_staged=False)),
     # long K: 64-column strips split to about 512 workgroups
     (4, 14336, 4096, dict(strip_cols=64, split_k=8, dense_waves=4, workgroups=512)),
 ])
