@@ -243,7 +243,8 @@ typedef struct {
 /* Sparse-path mappings (fq_problem.flags).  GATHER (M <= 4 only): each lane
  * decodes one 16-byte group and gathers X[m][k] from LDS for every row (VALU dot2).
  * MFMA: the tile's outliers are scattered into an LDS image of the MFMA B
- * operand and multiplied on the matrix cores.  Both are exact in fp32. */
+ * operand and multiplied on the matrix cores.  Both are exact in fp32.
+ * AUTO picks GATHER at M = 1 for by-column Tile-COO and MFMA otherwise. */
 enum { FQ_SPARSE_AUTO = 0, FQ_SPARSE_GATHER = 1, FQ_SPARSE_MFMA = 2, FQ_SPARSE_MASK = 3 };
 
 /* Schedule switches (fq_problem.flags), for ablation; the default is uniform
@@ -288,8 +289,9 @@ enum { FQ_SPARSE_WAVES = 64 };
 fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes);
 
 /*
- * fq_launch_config -- the launch the fused entry point would make for pr
- * (for tools and benchmarks; nothing is launched).  Outputs (host):
+ * fq_launch_config -- the launch the fused entry point would make for pr and
+ * a Tile-COO with the given buckets_per_tile (1..256) and group_mode (for
+ * tools and benchmarks; nothing is launched).  Outputs (host):
  *   cfg[0] strip width in columns (32 or 64)   cfg[1] K ranges per strip (split)
  *   cfg[2] dense waves per workgroup           cfg[3] outlier-only waves per workgroup
  *   cfg[4] outlier mapping (FQ_SPARSE_GATHER or FQ_SPARSE_MFMA)
@@ -297,10 +299,10 @@ fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes);
  *   cfg[7] dynamic LDS bytes per workgroup
  *   cfg[8] 1 when each tile's X slice is loaded row by row and reordered into
  *          MFMA operand order through LDS (MFMA mapping at 9..16 rows), else 0
- * buckets_per_tile is the Tile-COO's (1..256).
- * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_UNSUPPORTED.
+ * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_FORMAT (group_mode), FQ_ERR_UNSUPPORTED.
  */
-fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t cfg[9]);
+fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t group_mode,
+                           int32_t cfg[9]);
 
 /*
  * fq_w4a16_outlier_matmul -- fused Y = X dequant(W_Q) + X W_O in one kernel

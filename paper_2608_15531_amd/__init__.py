@@ -103,7 +103,8 @@ _SIGS = {
     "fq_debug_decode_tile_coo": ([C.POINTER(fq_tilecoo_dev), C.c_int32, C.c_int32, _P, _P, _P,
                                   _P], C.c_int),
     "fq_status_string": ([C.c_int], C.c_char_p),
-    "fq_launch_config": ([C.POINTER(fq_problem), C.c_int32, C.POINTER(C.c_int32)], C.c_int),
+    "fq_launch_config": ([C.POINTER(fq_problem), C.c_int32, C.c_int32, C.POINTER(C.c_int32)],
+                         C.c_int),
     "fq_quantize_outlier_aware": ([C.c_int32, C.c_int32, _P, C.c_int32, C.c_double,
                                    C.POINTER(C.c_int64), _P, _P, _P, _P, _P, _P], C.c_int),
     "fq_fill_padding_slots": ([C.c_int32, C.c_int32, _P, C.c_int32,
@@ -428,12 +429,13 @@ def fq_debug_decode_tile_coo(tc: TileCOODevice, K: int, N: int, stream=None):
 
 
 def fq_launch_config(M: int, K: int, N: int, split_k: int = 0, sparse: str = "auto",
-                     flags: int = 0, buckets_per_tile: int = 16) -> dict:
+                     flags: int = 0, buckets_per_tile: int = 16, group_mode: int = 0) -> dict:
     """The launch the fused entry point would make (nothing is launched)."""
     lib = load()
     pr = _problem(M, K, N, FQ_Y_BF16, split_k, 128, sparse, flags)
     cfg = (C.c_int32 * 9)()
-    _check(lib.fq_launch_config(C.byref(pr), buckets_per_tile, cfg), "fq_launch_config")
+    _check(lib.fq_launch_config(C.byref(pr), buckets_per_tile, group_mode, cfg),
+           "fq_launch_config")
     return {"strip_cols": cfg[0], "split_k": cfg[1], "dense_waves": cfg[2],
             "outlier_waves": cfg[3], "mapping": "gather" if cfg[4] == FQ_SPARSE_GATHER else "mfma",
             "workgroups": cfg[5], "stream_k": bool(cfg[6]), "lds_bytes": cfg[7],

@@ -54,13 +54,23 @@ fq_status check_tc(const fq_problem* pr, const fq_tilecoo_dev* tc) {
 
 int plan_opts(const fq_problem* pr);
 
+// Sparse mapping for make_plan: the caller's, else -1 (by M) -- except that
+// groups whose slots may lie in different columns (by-bucket grouping) always
+// take the MFMA mapping, which scatters every slot on its own; the gather
+// mapping is built around single-column groups.
+int plan_mode(const fq_problem* pr, int32_t group_mode) {
+  const int mapping = pr->flags & FQ_SPARSE_MASK;
+  if (mapping == FQ_SPARSE_GATHER) return 0;
+  if (mapping == FQ_SPARSE_MFMA || group_mode == FQ_GROUP_BY_BUCKET) return 1;
+  return -1;
+}
+
 fq_status run(const fq_problem* pr, const uint16_t* X, const uint32_t* Wq,
               const uint16_t* scales, const uint32_t* zeros, const fq_tilecoo_dev* tc, void* Y,
               void* workspace, size_t workspace_bytes, void* stream, bool dense, bool sparse,
               const float* y_addend) {
   fqi::Plan plan;
-  const int mapping = pr->flags & FQ_SPARSE_MASK;
-  const int mode = mapping == FQ_SPARSE_GATHER ? 0 : mapping == FQ_SPARSE_MFMA ? 1 : -1;
+  const int mode = plan_mode(pr, sparse ? tc->params.group_mode : FQ_GROUP_BY_COLUMN);
   if (!fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, dense, sparse,
                       sparse ? tc->params.buckets_per_tile : 0,
                       sparse ? tc->max_tile_groups : 0, &plan, mode, plan_opts(pr)))
@@ -116,12 +126,13 @@ const char* fq_status_string(fq_status s) {
   return "unknown status";
 }
 
-fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t cfg[9]) {
+fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t group_mode,
+                           int32_t cfg[9]) {
   if (!cfg) return FQ_ERR_NULL;
   fq_status st = check_problem(pr);
   if (st != FQ_OK) return st;
-  const int mapping = pr->flags & FQ_SPARSE_MASK;
-  const int mode = mapping == FQ_SPARSE_GATHER ? 0 : mapping == FQ_SPARSE_MFMA ? 1 : -1;
+  if (group_mode != FQ_GROUP_BY_COLUMN && group_mode != FQ_GROUP_BY_BUCKET) return FQ_ERR_FORMAT;
+  const int mode = plan_mode(pr, group_mode);
   fqi::Plan pl;
   if (!fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, true, true, buckets_per_tile, 0, &pl, mode,
                       plan_opts(pr)))

@@ -125,6 +125,8 @@ EXACT_CASES = [
     (4, 512, 128, 0.0, 0, c_params()),
     # nine rows: the smallest M whose X slice goes through the LDS stage
     (9, 1152, 448, 0.03, 0, c_params()),
+    # one row with by-bucket groups: the default mapping is MFMA here
+    (1, 2048, 1024, 0.02, 0, c_params(group_mode=1)),
     # more than 32 rows: 32-row slabs in the grid, ragged last slab, split-K
     (33, 1024, 256, 0.02, 0, c_params()),
     (64, 2048, 512, 0.01, 3, c_params()),

@@ -363,5 +363,12 @@ def test_launch_config_switches(lib):
     assert ew["outlier_waves"] == ew["dense_waves"] // 2
     assert fq.fq_launch_config(4, 4096, 28672, flags=fq.FQ_SCHED_STREAM_K)["stream_k"]
     assert fq.fq_launch_config(4, 4096, 4096, split_k=3)["split_k"] == 3
+    # groups spanning columns (by-bucket) take the MFMA mapping at M = 1 too
+    assert fq.fq_launch_config(1, 4096, 28672)["mapping"] == "gather"
+    assert fq.fq_launch_config(1, 4096, 28672, group_mode=fq.FQ_GROUP_BY_BUCKET)["mapping"] == "mfma"
+    assert fq.fq_launch_config(1, 4096, 28672, sparse="gather",
+                               group_mode=fq.FQ_GROUP_BY_BUCKET)["mapping"] == "gather"
+    with pytest.raises(fq.FqError):
+        fq.fq_launch_config(1, 4096, 4096, group_mode=2)
     with pytest.raises(fq.FqError):
         fq.fq_launch_config(5, 4096, 4096, sparse="gather")
