@@ -999,10 +999,11 @@ int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
 //    256-byte ones), no split, eight waves -- a cross-workgroup split-K
 //    reduction costs three dependent trips through the device-coherent
 //    memory level (about 2 us), more than the extra instructions per byte of
-//    the narrower strip.  With 12 or more rows the per-tile work is heavier
-//    and covering every CU pays, unless the 32-column strips already give
-//    192 workgroups of at most 32 tiles: 64-column strips split to at least
-//    256 workgroups, four waves.
+//    the narrower strip.  This holds up to 16 rows, where X goes through the
+//    LDS stage.  With two 16-row blocks (17..32 rows) the per-tile work is
+//    heavier and covering every CU pays, unless the 32-column strips already
+//    give 192 workgroups of at most 32 tiles: 64-column strips split to at
+//    least 256 workgroups, four waves.
 //  * Long K (down): 64-column strips split to about 512 workgroups, four
 //    waves.
 struct Shape {
@@ -1013,7 +1014,7 @@ Shape default_shape(int T, int N, int n_slabs, int slab_M) {
   if (units64 >= 160) return {4, 0, 0};
   int S = 1;
   if (T <= 64) {
-    if (slab_M >= 12 && (units32 < 192 || T > 32)) {
+    if (slab_M > 16 && (units32 < 192 || T > 32)) {
       while (units64 * S < 256 && 2 * S <= T / 8) S *= 2;
       return {4, S, 4};
     }

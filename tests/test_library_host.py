@@ -335,8 +335,10 @@ def test_debug_decode_rejects(lib):
     # narrow, K <= 8192: 32-column strips without split-K
     (1, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, mapping="mfma")),
     (8, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_staged=False)),
-    # few strips and 12+ rows: 64-column strips split to 256 workgroups, four waves
-    (16, 4096, 4096, dict(strip_cols=64, split_k=4, dense_waves=4, workgroups=256)),
+    # few strips, up to 16 rows: 32-column strips, no split
+    (16, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, workgroups=128)),
+    # few strips and two 16-row blocks: 64-column strips split to 256 workgroups, four waves
+    (32, 4096, 4096, dict(strip_cols=64, split_k=4, dense_waves=4, workgroups=256)),
     # 32-column strips already give 192 workgroups of 32 tiles: no split
     (16, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_staged=True)),
     # X slices through the LDS stage from 9 rows to one 16-row block
