@@ -689,12 +689,8 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
     // same exact count everywhere: the (D-1) NL loads of the following tiles
     // stay in flight.  Only the first tile's group loads wait for
     // tile_indptr, while its dense loads are already out.
-    //
-    // Code size is part of the cost: the instruction cache starts cold at
-    // every launch and each KB of code run for the first time costs about
-    // 0.4 us, so the loop body holds exactly one copy of the tile code per
-    // register buffer and the last partial round is predicated rather than
-    // peeled.
+    // The loop body holds one copy of the tile code per register buffer; the
+    // last partial round is predicated, not peeled.
     constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
     constexpr int D = pipeline_depth<MB, NCB>();
     TileRegs<MB, MODE, NCB> rg[D];
