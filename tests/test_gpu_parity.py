@@ -127,6 +127,8 @@ EXACT_CASES = [
     (9, 1152, 448, 0.03, 0, c_params()),
     # one row with by-bucket groups: the default mapping is MFMA here
     (1, 2048, 1024, 0.02, 0, c_params(group_mode=1)),
+    # the packing this kernel runs fastest on: by-bucket groups, one bucket per tile
+    (8, 1024, 512, 0.02, 0, c_params(group_mode=1, buckets_per_tile=1)),
     # more than 32 rows: 32-row slabs in the grid, ragged last slab, split-K
     (33, 1024, 256, 0.02, 0, c_params()),
     (64, 2048, 512, 0.01, 3, c_params()),
