@@ -37,14 +37,34 @@ __device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
 
 constexpr float kCodeOffset = 128.f;   // value of the bf16 bit pattern 0x4300
 
-__device__ __forceinline__ bf16x8_t dequant_word(uint32_t w) {
+// Two words (two columns) at once, each into its 8-element operand: the
+// and-or above on the word shifted by 0, 4, 8 and 12.  One 64-bit shift of
+// the pair (w1:w0) yields w1 >> s in its high half and w0 >> s in its low
+// half, polluted only in bits 32-s..31 by w1's low bits, which the nibble mask
+// clears for s <= 12, so three 64-bit shifts replace six 32-bit ones (4.5
+// against 2 x 3.1 cycles measured per instruction).
+template <int S>
+__device__ __forceinline__ uint64_t shr64c(uint64_t p) {
+  uint64_t r;
+  asm("v_lshrrev_b64 %0, %2, %1" : "=v"(r) : "v"(p), "i"(S));
+  return r;
+}
+
+__device__ __forceinline__ void dequant_pair(uint32_t w0, uint32_t w1, bf16x8_t& b0, bf16x8_t& b1) {
   const uint32_t mask = 0x000F000Fu, bias = 0x43004300u;
-  u32x4_t r;
-  r[0] = and_or(w, mask, bias);
-  r[1] = and_or(w >> 4, mask, bias);
-  r[2] = and_or(w >> 8, mask, bias);
-  r[3] = and_or(w >> 12, mask, bias);
-  return __builtin_bit_cast(bf16x8_t, r);
+  const uint64_t p = (uint64_t(w1) << 32) | w0;
+  const uint64_t s4 = shr64c<4>(p), s8 = shr64c<8>(p), s12 = shr64c<12>(p);
+  u32x4_t r0, r1;
+  r0[0] = and_or(w0, mask, bias);
+  r1[0] = and_or(w1, mask, bias);
+  r0[1] = and_or(uint32_t(s4), mask, bias);
+  r1[1] = and_or(uint32_t(s4 >> 32), mask, bias);
+  r0[2] = and_or(uint32_t(s8), mask, bias);
+  r1[2] = and_or(uint32_t(s8 >> 32), mask, bias);
+  r0[3] = and_or(uint32_t(s12), mask, bias);
+  r1[3] = and_or(uint32_t(s12 >> 32), mask, bias);
+  b0 = __builtin_bit_cast(bf16x8_t, r0);
+  b1 = __builtin_bit_cast(bf16x8_t, r1);
 }
 
 // Position of element k%8 inside an 8-element chunk of the LDS activation

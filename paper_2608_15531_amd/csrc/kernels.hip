@@ -573,11 +573,14 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
             w4[0] = cur.w[step].x; w4[1] = cur.w[step].y;
           }
   #pragma unroll
-          for (int c = 0; c < NCB; ++c) {
-            const bf16x8_t Bq = dequant_word(w4[c]);
+          for (int c = 0; c < NCB; c += 2) {
+            bf16x8_t Bq[2];
+            dequant_pair(w4[c], w4[c + 1], Bq[0], Bq[1]);
   #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-              tmp[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bq, tmp[mb][c], 0, 0, 0);
+            for (int e = 0; e < 2; ++e)
+  #pragma unroll
+              for (int mb = 0; mb < MB; ++mb)
+                tmp[mb][c + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bq[e], tmp[mb][c + e], 0, 0, 0);
           }
   #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
@@ -614,14 +617,18 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
       }
 
       // ---- sparse path, MFMA mapping: scatter the tile's outliers into the
-      // image, read it back per step and multiply into the output tile
+      // image, read it back per step and multiply into the output tile.
+      // Every lane scatters (and later clears): lanes past the tile's last
+      // group hold that group again and rewrite the same values at the same
+      // places, so only an empty tile (whose loaded group is not its own)
+      // is skipped -- a wave-uniform branch, no per-lane masking.
       uint32_t n_g = 0;
       if (SPARSE) n_g = cur.g1 - cur.g0;
       uint32_t addr[2][4];
       if (SPM) {
   #pragma unroll
         for (int j = 0; j < 2; ++j)
-          if (uint32_t(lane + 64 * j) < n_g) scatter_group<NCB>(img, trash, cur.g[j], half, addr[j]);
+          if (n_g > 64u * j) scatter_group<NCB>(img, trash, cur.g[j], half, addr[j]);
         for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
           uint32_t ad[4];
           scatter_group<NCB>(img, trash, a.packed[cur.g0 + gi], half, ad);
@@ -657,7 +664,7 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
         __builtin_amdgcn_wave_barrier();
   #pragma unroll
         for (int j = 0; j < 2; ++j)
-          if (uint32_t(lane + 64 * j) < n_g) clear_group(addr[j]);
+          if (n_g > 64u * j) clear_group(addr[j]);
         for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
           uint32_t o01, o23;
           const uint4 raw = a.packed[cur.g0 + gi];
