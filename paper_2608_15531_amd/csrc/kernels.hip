@@ -1,42 +1,45 @@
 // Fused outlier-aware W4A16 decode matmul for MI355X (gfx950), its unfused
 // halves, and the Tile-COO group decoder.
 //
-// One workgroup = four wave64 = one 64-column output strip x one contiguous K
-// range of 128-row tiles (FlashQuant Sec. 3.1, CTA level: the dense and the
-// sparse work of the same output tile run in the same workgroup and
-// accumulate into the same register output tile).  Each wave streams its own
-// contiguous run of tiles with no workgroup barrier in the loop.
+// One workgroup = NW wave64 (4 or 8) = one output strip of 32 or 64 columns
+// (NCB = 2 or 4 MFMA column blocks) x one contiguous K range of 128-row tiles
+// (FlashQuant Sec. 3.1, CTA level: the dense and the sparse work of the same
+// output tile run in the same workgroup and accumulate into the same register
+// output tile).  Each wave streams its own contiguous run of tiles with no
+// workgroup barrier in the loop.
 //
-//   prefetch  two register buffers alternate, each holding one tile: 16 bytes
-//             of packed INT4 per lane and 32-row step (one 128-bit load each),
-//             the fp16 scales and INT4 zero-points of the lane's four columns,
+//   prefetch  two register buffers alternate, each holding one tile: 4 NCB
+//             bytes of packed INT4 per lane and 32-row step (one load each),
+//             the fp16 scales and INT4 zero-points of the lane's NCB columns,
 //             the tile's slice of X (from L2), and the tile's Tile-COO groups,
 //             one 16-byte group per lane (the tiles of a strip are stored
 //             contiguously, so one load of tile_indptr gives every range).
 //             While tile t is computed, tile t+1 is in flight (Sec. 4.1).
-//   dense     per 32-row step a lane turns 8 codes of each of its 4 columns
+//             With 9..16 rows the X slice is loaded row-wise and reordered
+//             through a per-wave LDS stage (template flag XSTAGE).
+//   dense     per 32-row step a lane turns 8 codes of each of its NCB columns
 //             into bf16 (128 + q) operands in registers and issues
 //             v_mfma_f32_16x16x32_bf16 against X; one more MFMA against an
 //             all-ones operand yields the per-row sums of X.  After the group:
 //             acc += s * (sum x (128+q) - (128+z) sum x), i.e. eq. (3) applied
 //             once per (group, column) in fp32.
 //   sparse    (Sec. 3.1 thread level, Sec. 4.2 decoding) two mappings of the
-//             same Tile-COO groups, chosen by the number of rows M:
-//     M = 1   the tile's X slice sits in the wave's LDS slot; each lane decodes
-//             one group, gathers X[m][k] for every row and accumulates v * x
-//             with v_dot2_f32_bf16 into the wave's LDS output buffer (the
-//             mapping also serves M <= 4 on request).
-//     M >= 2  each lane scatters its group's values into an LDS buffer laid out
-//             as the MFMA B operand of the tile (zero elsewhere); per 32-row
-//             step the wave reads the step's four blocks back with
-//             conflict-free 128-bit reads and issues four MFMAs against the
-//             same X fragments straight into the register output tile; the
-//             zeros are restored after the tile.  bf16 x bf16 products are
-//             exact in the fp32 accumulator, so this is the SpMM of eq. (1) on
-//             the matrix cores, with its cost independent of M.  When the
-//             strips fit the CUs this kernel runs eight waves per workgroup.
-//   reduce    after the loop the four waves' register tiles (and sparse
-//             buffers) are summed in LDS in a fixed order.  With split-K each
+//             same Tile-COO groups:
+//     gather  (M = 1, by-column groups, 64-column strips; up to 4 rows on
+//             request) the tile's X slice sits in the wave's LDS slot; each
+//             lane decodes one group, gathers X[m][k] for every row and
+//             accumulates v * x with v_dot2_f32_bf16 into the wave's LDS output
+//             buffer.
+//     MFMA    (otherwise) each lane scatters its group's values into an LDS
+//             buffer laid out as the MFMA B operand of the tile (zero
+//             elsewhere); per 32-row step the wave reads the step's NCB blocks
+//             back with conflict-free 128-bit reads and issues NCB MFMAs
+//             against the same X fragments straight into the register output
+//             tile; the zeros are restored after the tile.  bf16 x bf16
+//             products are exact in the fp32 accumulator, so this is the SpMM
+//             of eq. (1) on the matrix cores, with its cost independent of M.
+//   reduce    after the loop the waves' register tiles (and sparse buffers)
+//             are summed in LDS in a fixed order.  With split-K each
 //             workgroup stores its fp32 partial with device-coherent stores
 //             and the last to arrive at the strip's counter adds all partials
 //             in split order and writes Y (Sec. 3.1 Stream-K reduction), then
