@@ -50,7 +50,7 @@ def kernel_name(fq, M, K, N):
     mb = 1 if min(M, 32) <= 16 else 2
     mode = 0 if c["mapping"] == "gather" else 1
     sk = "true" if c["stream_k"] else "false"
-    xs = "true" if c["x_staged"] else "false"
+    xs = c["x_stage_loads"]
     return (f"matmul_kernel<{mb}, {mode}, {c['strip_cols'] // 16}, true, true, "
             f"{c['dense_waves']}, {sk}, {c['outlier_waves']}, {xs}>")
 

@@ -302,8 +302,9 @@ fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes);
  *   cfg[4] outlier mapping (FQ_SPARSE_GATHER or FQ_SPARSE_MFMA)
  *   cfg[5] workgroups in the grid              cfg[6] 1 under Stream-K, else 0
  *   cfg[7] dynamic LDS bytes per workgroup
- *   cfg[8] 1 when each tile's X slice is loaded row by row and reordered into
- *          MFMA operand order through LDS (MFMA mapping at 9..16 rows), else 0
+ *   cfg[8] loads per tile of the X slice when it is loaded row-wise (4 rows per
+ *          load) and reordered into MFMA operand order through LDS: 1, 2 or 4
+ *          (ceil(M/4); the MFMA mapping with at most 16 rows), else 0
  * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_FORMAT (group_mode), FQ_ERR_UNSUPPORTED.
  */
 fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t group_mode,

@@ -439,7 +439,7 @@ def fq_launch_config(M: int, K: int, N: int, split_k: int = 0, sparse: str = "au
     return {"strip_cols": cfg[0], "split_k": cfg[1], "dense_waves": cfg[2],
             "outlier_waves": cfg[3], "mapping": "gather" if cfg[4] == FQ_SPARSE_GATHER else "mfma",
             "workgroups": cfg[5], "stream_k": bool(cfg[6]), "lds_bytes": cfg[7],
-            "x_staged": bool(cfg[8])}
+            "x_staged": bool(cfg[8]), "x_stage_loads": cfg[8]}
 
 
 def fq_workspace_bytes(M: int, K: int, N: int, y_dtype=FQ_Y_BF16, split_k: int = 0,

@@ -16,7 +16,6 @@ constexpr int kXStride = 136;   // LDS row stride (elements) of a staged 128-wid
 constexpr int kGatherMaxM = 1;  // up to this M the sparse path gathers X in LDS; above, MFMA
 constexpr int kGatherLimitM = 4; // rows the gather mapping can stage at all
 constexpr int kImageBytes = 16384;   // one wave's B-operand image of a 128 x 64 tile
-constexpr int kXStageMinM = 9;  // MFMA mapping, one 16-row block: X goes through LDS from here on
 // The workspace starts with a fixed counter region (one uint32 per output
 // strip, zero between calls) so that a workspace shared by problems of
 // different shapes never finds partial sums where a counter is expected.
@@ -42,7 +41,7 @@ struct Plan {
   int G;             // workgroups per slab
   int C;             // partial-sum slots per strip (most contributors to one strip)
   int B;             // buckets per tile
-  int XS;            // 1: X slices go through an LDS stage (MFMA mapping, 9..16 rows)
+  int XS;            // row-wise X loads per tile through the LDS stage: 0, or 1, 2, 4 (ceil(M/4))
   // dynamic LDS layout, bytes: one slot per wave (X slice or B-operand
   // image), then the gather-mode sparse output buffers or the X stages
   size_t slot_bytes, off_shc, off_flag, off_trash, off_xs, lds_bytes;

@@ -15,8 +15,9 @@
 //             one 16-byte group per lane (the tiles of a strip are stored
 //             contiguously, so one load of tile_indptr gives every range).
 //             While tile t is computed, tile t+1 is in flight (Sec. 4.1).
-//             With 9..16 rows the X slice is loaded row-wise and reordered
-//             through a per-wave LDS stage (template flag XSTAGE).
+//             With the MFMA mapping and one 16-row block the X slice is loaded
+//             row-wise, 4 rows per load, and reordered through a per-wave LDS
+//             stage (template parameter XR = loads per tile).
 //   dense     per 32-row step a lane turns 8 codes of each of its NCB columns
 //             into bf16 (128 + q) operands in registers and issues
 //             v_mfma_f32_16x16x32_bf16 against X; one more MFMA against an
@@ -89,9 +90,9 @@ struct MatmulArgs {
 };
 
 // Global loads one tile costs in each mode (each counts once in vmcnt).
-template <int MB, int MODE, bool DENSE, bool SPARSE>
+template <int MB, int MODE, bool DENSE, bool SPARSE, int XR>
 constexpr int loads_per_tile() {
-  return (DENSE ? 6 : 0) + (MODE == 0 ? 1 : 4 * MB) + (SPARSE ? 2 : 0);
+  return (DENSE ? 6 : 0) + (MODE == 0 ? 1 : XR > 0 ? XR : 4 * MB) + (SPARSE ? 2 : 0);
 }
 
 // Tiles in flight per wave.  Each buffer is one more copy of the tile code
@@ -150,12 +151,11 @@ struct Operands {
   uint32_t lx[4 * MB];   // X: MODE 0 chunk lane; MODE 1 see load_tile_dense
 };
 
-// X staging (template flag XSTAGE; MFMA mapping, one 16-row block, chosen from
-// 9 rows on): the tile's X slice is loaded row by row -- each load covers
-// 4 rows x 256 bytes, 8 whole cache lines, where loads in operand order touch
-// 16 half lines -- and reordered into operand order through a 4 KB stage in
-// LDS.  With fewer rows the operand-order loads touch few lines and the stage
-// only adds latency.
+// X staging (template parameter XR, MFMA mapping, one 16-row block): the
+// tile's X slice is loaded row-wise -- load j covers rows 4j..4j+3 x 256
+// bytes, whole cache lines, where loads in operand order touch up to 16 half
+// lines each -- XR = ceil(M / 4) loads (1, 2 or 4) instead of four, and
+// reordered into operand order through an XR KB stage in LDS.
 
 // The loads of a tile that do not depend on the Tile-COO offsets: packed
 // codes, scales and zero-points (dense path) and the tile's slice of X:
@@ -167,7 +167,7 @@ struct Operands {
 // counts outstanding loads exactly across the prefetch.  A wave-wide load of
 // one step covers 4 packed rows x (16 NCB) columns: 128-byte row segments for
 // 32-column strips, 256-byte ones for 64-column strips.
-template <int MB, int MODE, int NCB, bool DENSE, bool XSTAGE>
+template <int MB, int MODE, int NCB, bool DENSE, int XR>
 __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Operands<MB>& op,
                                                 int t, int n0, TileRegs<MB, MODE, NCB>& r) {
   if (DENSE) {
@@ -188,9 +188,9 @@ __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Opera
   const uint32_t xt = uint32_t(t) * 256u;
   if (MODE == 0) {
     r.x[0] = buf_load16(op.x, op.lx[0], xt);
-  } else if (XSTAGE) {
+  } else if (XR > 0) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) r.x[j] = buf_load16(op.x, op.lx[j], xt);
+    for (int j = 0; j < XR; ++j) r.x[j] = buf_load16(op.x, op.lx[j], xt);
   } else {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
@@ -381,10 +381,11 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
   for (int j = 0; j < 4; ++j) lds_store16(addr[j], 0u);
 }
 
-template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS, bool XSTAGE>
+template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS, int XR>
 __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args) {
   static_assert(NCB == 4 || (NCB == 2 && MODE == 1), "32-column strips use the MFMA outlier mapping");
-  static_assert(!XSTAGE || (MODE == 1 && MB == 1), "X staging: MFMA mapping, one 16-row block");
+  static_assert(XR == 0 || ((XR == 1 || XR == 2 || XR == 4) && MODE == 1 && MB == 1),
+                "X staging: 1, 2 or 4 row-wise loads, MFMA mapping, one 16-row block");
   // NWS > 0: warp specialisation (Sec. 3.1) -- NW dense waves and NWS outlier
   // waves share the strip's K range and the output reduction.
   constexpr int NT = NW + NWS;                 // waves per workgroup
@@ -478,9 +479,9 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
   if (MODE == 0) {
     // rows past M load row M-1 (the slice store below is then a rewrite)
     op.lx[0] = (uint32_t(min(lane >> 4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(lane & 15)) * 2u;
-  } else if (XSTAGE) {
+  } else if (XR > 0) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)   // rows past M load row M-1, never stored
+    for (int j = 0; j < XR; ++j)   // rows past M load row M-1, never read
       op.lx[j] = (uint32_t(min(4 * j + h, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(c4)) * 2u;
   } else {
 #pragma unroll
@@ -488,11 +489,11 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
       op.lx[mb] = (uint32_t(min(mb * 16 + c4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(h)) * 2u;
   }
   const uint32_t img = lds_address(bo);                  // this wave's image
-  // X stage of this wave (16 rows x 256 bytes, 16-byte chunk q of row r at
+  // X stage of this wave (4 XR rows x 256 bytes, 16-byte chunk q of row r at
   // position q ^ r); its first 16 bytes double as the trash word, written by
   // the scatter only between the stage's read and its next write
-  unsigned char* xst = smem + a.off_xs + size_t(wave) * 4096;
-  const uint32_t trash = lds_address(XSTAGE ? xst : smem + a.off_trash);
+  unsigned char* xst = smem + a.off_xs + size_t(wave) * (1024 * XR);
+  const uint32_t trash = lds_address(XR > 0 ? xst : smem + a.off_trash);
 
 
   // The current segment (read by the lambdas below).
@@ -517,7 +518,7 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
       load_tile_sparse<MB, MODE, NCB, SPARSE>(op, lane, g0, g1, r);
     };
     auto issue = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
-      load_tile_dense<MB, MODE, NCB, DENSE, XSTAGE>(a, op, t, n0, r);
+      load_tile_dense<MB, MODE, NCB, DENSE, XR>(a, op, t, n0, r);
       issue_sparse(t, r);
     };
 
@@ -534,18 +535,20 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
   #pragma unroll
         for (int step = 0; step < 4; ++step)
           A[0][step] = *reinterpret_cast<const bf16x8_t*>(xs + min(c4, a.M - 1) * kXRow + step * 32 + 8 * h);
-      } else if (XSTAGE) {
+      } else if (XR > 0) {
         // load j of lane (c4, h) holds chunk c4 of row 4j + h; fragment
-        // `step` of lane (c4, h) is chunk 4 step + h of row c4.  Both
-        // directions touch 16 distinct 16-byte bank groups per 16 lanes.
+        // `step` of lane (c4, h) is chunk 4 step + h of row c4 (rows past M
+        // read row M-1, which is staged).  Both directions touch 16 distinct
+        // 16-byte bank groups per 16 lanes.
   #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < XR; ++j)
           *reinterpret_cast<uint4*>(xst + (4 * j + h) * 256 + ((c4 ^ (4 * j + h)) << 4)) = cur.x[j];
         __builtin_amdgcn_wave_barrier();
+        const int rr = min(c4, a.M - 1);
   #pragma unroll
         for (int step = 0; step < 4; ++step)
           A[0][step] = __builtin_bit_cast(bf16x8_t, permute_chunk(*reinterpret_cast<const uint4*>(
-                                                        xst + c4 * 256 + (((4 * step + h) ^ c4) << 4))));
+                                                        xst + rr * 256 + (((4 * step + h) ^ rr) << 4))));
       } else {
   #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
@@ -701,7 +704,7 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
     // tile_indptr, while its dense loads are already out.
     // The loop body holds one copy of the tile code per register buffer; the
     // last partial round is predicated, not peeled.
-    constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE>();
+    constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE, XR>();
     constexpr int D = pipeline_depth<MB, NCB>();
     TileRegs<MB, MODE, NCB> rg[D];
     if (w_lo < w_hi) {
@@ -906,9 +909,9 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
   }
 }
 
-template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK, int NWS, bool XSTAGE>
+template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK, int NWS, int XR>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XSTAGE>;
+  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR>;
   if (pl.lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -920,23 +923,25 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
   return int(hipGetLastError());
 }
 
-template <int MB, int MODE, int NCB, int NW, bool SK, bool XSTAGE>
+template <int MB, int MODE, int NCB, int NW, bool SK, int XR>
 int launch_roles(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
   if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8)) {
     if (dense && sparse && pl.NWS > 0)
-      return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2, XSTAGE>(pl, a, s);
+      return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2, XR>(pl, a, s);
   }
-  if (dense && sparse) return launch_variant<MB, MODE, NCB, true, true, NW, SK, 0, XSTAGE>(pl, a, s);
-  if (dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK, 0, XSTAGE>(pl, a, s);
-  return launch_variant<MB, MODE, NCB, false, true, NW, SK, 0, XSTAGE>(pl, a, s);
+  if (dense && sparse) return launch_variant<MB, MODE, NCB, true, true, NW, SK, 0, XR>(pl, a, s);
+  if (dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK, 0, XR>(pl, a, s);
+  return launch_variant<MB, MODE, NCB, false, true, NW, SK, 0, XR>(pl, a, s);
 }
 
 template <int MB, int MODE, int NCB, int NW, bool SK>
 int launch_sched(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
   if constexpr (MODE == 1 && MB == 1) {
-    if (pl.XS) return launch_roles<MB, MODE, NCB, NW, SK, true>(pl, a, dense, sparse, s);
+    if (pl.XS == 4) return launch_roles<MB, MODE, NCB, NW, SK, 4>(pl, a, dense, sparse, s);
+    if (pl.XS == 2) return launch_roles<MB, MODE, NCB, NW, SK, 2>(pl, a, dense, sparse, s);
+    if (pl.XS == 1) return launch_roles<MB, MODE, NCB, NW, SK, 1>(pl, a, dense, sparse, s);
   }
-  return launch_roles<MB, MODE, NCB, NW, SK, false>(pl, a, dense, sparse, s);
+  return launch_roles<MB, MODE, NCB, NW, SK, 0>(pl, a, dense, sparse, s);
 }
 
 // Stream-K is built for 64-column strips only (the plan never combines it
@@ -1006,7 +1011,7 @@ int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
 //    reduction costs three dependent trips through the device-coherent
 //    memory level (about 2 us), more than the extra instructions per byte of
 //    the narrower strip.  This holds up to 16 rows, where X goes through the
-//    LDS stage.  With two 16-row blocks (17..32 rows) the per-tile work is
+//    LDS stage (measured at 9..16 rows).  With two 16-row blocks (17..32 rows) the per-tile work is
 //    heavier and covering every CU pays, unless the 32-column strips already
 //    give 192 workgroups of at most 32 tiles: 64-column strips split to at
 //    least 256 workgroups, four waves.
@@ -1140,14 +1145,16 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   // reduction buffer (one tile per wave) reuses them
   const int n_slots = p.NWS > 0 ? p.NWS : p.NW;
   const size_t red_bytes = size_t(p.NW + p.NWS) * p.slab_M * (16 * p.NCB) * 4;
-  p.XS = p.MODE == 1 && p.MB == 1 && p.slab_M >= kXStageMinM;
+  // X staging with the MFMA mapping and one 16-row block: ceil(M / 4)
+  // row-wise loads per tile (1, 2 or 4)
+  p.XS = (p.MODE == 1 && p.MB == 1) ? (p.slab_M <= 4 ? 1 : p.slab_M <= 8 ? 2 : 4) : 0;
   if (p.XS) {
-    // images, then a 4 KB X stage per wave.  After the tile loop the
+    // images, then an XS KB X stage per wave.  After the tile loop the
     // reduction buffer reuses them, and the split-K flag sits at the head of
     // wave 0's stage when the reduction buffer ends before it.  Each wave's
     // trash word is the head of its own stage.
     p.off_xs = n_slots * p.slot_bytes;
-    const size_t end = std::max(p.off_xs + size_t(p.NW + p.NWS) * 4096, red_bytes);
+    const size_t end = std::max(p.off_xs + size_t(p.NW + p.NWS) * 1024 * p.XS, red_bytes);
     p.off_shc = end;
     p.off_trash = p.off_xs;
     if (red_bytes <= p.off_xs) {

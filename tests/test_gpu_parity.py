@@ -123,7 +123,7 @@ EXACT_CASES = [
     (8, 128, 64, 0.5, 0, c_params()),
     (2, 256, 64, 1.0, 0, c_params(buckets_per_tile=4)),
     (4, 512, 128, 0.0, 0, c_params()),
-    # nine rows: the smallest M whose X slice goes through the LDS stage
+    # nine rows: the smallest M whose X slice takes four row-wise loads through the LDS stage
     (9, 1152, 448, 0.03, 0, c_params()),
     # one row with by-bucket groups: the default mapping is MFMA here
     (1, 2048, 1024, 0.02, 0, c_params(group_mode=1)),

@@ -331,22 +331,26 @@ def test_debug_decode_rejects(lib):
 @pytest.mark.parametrize("M,K,N,expect", [
     # wide matrices: 64-column strips, no split; the gather mapping at M = 1
     (1, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="gather")),
-    (16, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="mfma", x_staged=True)),
+    (16, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="mfma", x_stage_loads=4)),
     # narrow, K <= 8192: 32-column strips without split-K
-    (1, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, mapping="mfma")),
-    (8, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_staged=False)),
+    (1, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, mapping="mfma", x_stage_loads=1)),
+    (8, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_stage_loads=2)),
     # few strips, up to 16 rows: 32-column strips, no split
     (16, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, workgroups=128)),
     # few strips and two 16-row blocks: 64-column strips split to 256 workgroups, four waves
     (32, 4096, 4096, dict(strip_cols=64, split_k=4, dense_waves=4, workgroups=256)),
     # 32-column strips already give 192 workgroups of 32 tiles: no split
-    (16, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_staged=True)),
-    # X slices through the LDS stage from 9 rows to one 16-row block
-    (9, 4096, 6144, dict(x_staged=True)),
-    (17, 4096, 6144, dict(x_staged=False)),
+    (16, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_stage_loads=4)),
+    # X slices through the LDS stage with ceil(M/4) row-wise loads, one 16-row block
+    (4, 4096, 6144, dict(x_stage_loads=1)),
+    (5, 4096, 6144, dict(x_stage_loads=2)),
+    (9, 4096, 6144, dict(x_stage_loads=4)),
+    (17, 4096, 6144, dict(x_staged=False, x_stage_loads=0)),
     # 160+ 64-column strips: 64-column strips, no split, eight waves
     (8, 4096, 14336, dict(strip_cols=64, split_k=1, dense_waves=8)),
     (1, 8192, 10240, dict(strip_cols=64, mapping="gather", x_staged=False)),
+    # the gather mapping stages its own X slice
+    (1, 4096, 28672, dict(mapping="gather", x_stage_loads=0)),
     # long K: 64-column strips split to about 512 workgroups
     (4, 14336, 4096, dict(strip_cols=64, split_k=8, dense_waves=4, workgroups=512)),
 ])
