@@ -322,6 +322,63 @@ def mfma_flops(fq, M, K, N):
     return slabs * mb * (N // c["strip_cols"]) * (K // 128) * per_tile * 16 * 16 * 32 * 2
 
 
+LARGE_M_CASES = [(4096, 14336, M) for M in (32, 64, 128)] + [(14336, 4096, M) for M in (32, 64, 128)]
+
+
+def pmc_pass_large_m(fq, torch, dev, launches=4):
+    """Eager fused launches of the larger-M cases, in a fixed order, for a
+    rocprofv3 --pmc run of the MFMA counters (one JSON line names them)."""
+    from synth import make_activations, make_problem, seed_for
+    order = []
+    for si, (K, N, M) in enumerate(LARGE_M_CASES):
+        p = make_problem(1, K, N, frac=FRAC, seed=seed_for(4, si, 0))
+        host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v)
+        Wq, s, z = fq.to_device(p, dev)[1:]
+        tc = fq.TileCOODevice(host, dev)
+        x = torch.from_numpy(make_activations(M, K, seed_for(4, si, 1)).view(np.int16).copy())
+        x = x.view(torch.bfloat16).to(dev)
+        for _ in range(launches):
+            fq.fq_w4a16_outlier_matmul(x, Wq, s, z, tc)
+        torch.cuda.synchronize()
+        order.append({"K": K, "N": N, "M": M, "launches": launches,
+                      "kernel": kernel_name(fq, M, K, N), "flops": mfma_flops(fq, M, K, N)})
+    print(json.dumps({"pmc_large_m": order}), flush=True)
+
+
+def pmc_summary_mfma(csv_path, log_path):
+    """MFMA counters of a --pmc-pass-large-m run (MfmaUtil, MfmaFlopsBF16) as a
+    markdown table.  No GPU needed."""
+    import csv
+    meta = None
+    with open(log_path) as fh:
+        for line in fh:
+            if line.startswith('{"pmc_large_m"'):
+                meta = json.loads(line)["pmc_large_m"]
+    if meta is None:
+        raise SystemExit(f"no pmc_large_m line in {log_path}")
+    rows = {}
+    for r in csv.DictReader(open(csv_path)):
+        if "matmul_kernel" not in r["Kernel_Name"]:
+            continue
+        d = rows.setdefault(int(r["Dispatch_Id"]), {})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    disp = [rows[k] for k in sorted(rows)]
+    if len(disp) != sum(c["launches"] for c in meta):
+        raise SystemExit(f"{len(disp)} matmul dispatches in the CSV, expected "
+                         f"{sum(c['launches'] for c in meta)}")
+    out = ["| K x N | M | kernel | MfmaUtil % (counter) | MFMA bf16 FLOPs per launch (counter) | "
+           "MFMA FLOPs per launch (model) |", "|---|---|---|---|---|---|"]
+    i = 0
+    for c in meta:
+        ds = disp[i:i + c["launches"]]
+        i += c["launches"]
+        util = sum(d["MfmaUtil"] for d in ds) / len(ds)
+        fl = sum(d["MfmaFlopsBF16"] for d in ds) / len(ds)
+        out.append(f"| {c['K']}x{c['N']} | {c['M']} | `{c['kernel']}` | {util:.1f} | {fl:.4g} | "
+                   f"{c['flops']:.4g} |")
+    print("\n".join(out))
+
+
 def sweep(fq, torch, which, dev, copies_min=4):
     """Per-matmul timings of the other workloads (not the step): the density
     and structure sweep, the Llama-3-70B decode layer, and the larger-M
@@ -453,6 +510,11 @@ def main():
                     help="no step timing: per-matmul timings of the density / structure "
                          "sweep (M=8, 4096x14336), the Llama-3-70B decode linears (M=1..32) "
                          "or the larger-M crossover (M=32..128, with MFMA utilisation)")
+    ap.add_argument("--pmc-pass-large-m", action="store_true",
+                    help="eager fused launches of the larger-M cases for a rocprofv3 --pmc "
+                         "run of MfmaUtil / MfmaFlopsBF16")
+    ap.add_argument("--pmc-summary-mfma", nargs=2, metavar=("CSV", "LOG"),
+                    help="no GPU: summarise a --pmc-pass-large-m counter CSV")
     ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "SQ_CSV", "LOG"),
                     help="no GPU: summarise the rocprofv3 counter CSVs of --pmc-pass runs "
                          "(SQ_CSV may be '-') into the traffic profile text")
@@ -460,6 +522,9 @@ def main():
     if args.pmc_summary:
         fcsv, wcsv, sqcsv, logp = args.pmc_summary
         pmc_summary(fcsv, wcsv, None if sqcsv == "-" else sqcsv, logp)
+        return
+    if args.pmc_summary_mfma:
+        pmc_summary_mfma(*args.pmc_summary_mfma)
         return
 
     if args.gpus != 1:
@@ -478,6 +543,9 @@ def main():
     R = args.copies
     if args.sweep:
         sweep(fq, torch, args.sweep, dev)
+        return
+    if args.pmc_pass_large_m:
+        pmc_pass_large_m(fq, torch, dev)
         return
 
     # ---------------------------------------------------------- inputs
