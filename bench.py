@@ -699,6 +699,7 @@ def main():
         us = per_launch_us(c, "fused", reps)
         fused_total_us += us
         d = {"shape": c.name, "M": c.M, "K": c.K, "N": c.N, "bytes": c.bytes,
+             "tilecoo_bytes": c.tcs[0].nbytes, "tilecoo_min_bytes": 4 * int(c.tcs[0].sizes.nnz),
              "kernel": kernel_name(fq, c.M, c.K, c.N),
              "fused_us": round(us, 3), "fused_GBs": round(c.bytes / us / 1e3, 1),
              "pct_peak": round(100 * c.bytes / us / 1e3 / HBM_PEAK_GBS, 1)}
@@ -730,6 +731,8 @@ def main():
                 torch.cuda.synchronize()
                 us = e0.elapsed_time(e1) * 1e3 / (reps * copies)
                 d["bf16_gemm_us"] = round(us, 3)
+                # the GEMM's own algorithmic bytes: bf16 W, X and Y
+                d["bf16_gemm_GBs"] = round((2 * K * N + 2 * d["M"] * K + 2 * d["M"] * N) / us / 1e3, 1)
                 d["speedup_vs_bf16_gemm"] = round(us / d["fused_us"], 3)
             del Ws
             torch.cuda.empty_cache()
