@@ -200,6 +200,60 @@ def test_exact_split_k_both_strip_widths(gpu_lib, case, strip):
     assert np.array_equal(yd, ref(prob, dense_only=True).astype(np.float32))
 
 
+def _column_pattern_problem(M, counts, seed):
+    """Exact-arithmetic problem (K = 256, N = 128) whose first 128 x 64 tile
+    holds counts[c] outliers in column c (rows spread over the tile), the other
+    tiles a few each; values +-j/8 as in make_exact_problem."""
+    prob = make_exact_problem(M, 256, 128, frac=0.0, seed=seed)
+    rng = np.random.Generator(np.random.PCG64(seed + 1))
+    ks, ns = [], []
+    for c, cnt in enumerate(counts):
+        rows = rng.choice(128, size=cnt, replace=False)
+        ks += list(rows)
+        ns += [c] * cnt
+    for t_k, t_n in ((1, 0), (0, 1), (1, 1)):   # the other tiles: 3 outliers each
+        rows = rng.choice(128, size=3, replace=False)
+        ks += list(t_k * 128 + rows)
+        ns += list(t_n * 64 + rng.choice(64, size=3, replace=False))
+    k = np.array(ks, dtype=np.int32)
+    n = np.array(ns, dtype=np.int32)
+    mags = rng.integers(1, 33, size=k.size).astype(np.float32) / 8.0
+    signs = np.where(rng.integers(0, 2, size=k.size) == 1, -1.0, 1.0).astype(np.float32)
+    from synth import bf16_bits_from_f32
+    return dataclasses.replace(prob, k=k, n=n, v=bf16_bits_from_f32(mags * signs))
+
+
+# by-column groups in the first tile: 64 (one load pass), 65 (second pass),
+# 128 (both passes full), 129 and 200 (the loop past the preloaded groups)
+GROUP_COUNT_CASES = {
+    64: [1] * 64,
+    65: [5] + [1] * 63,
+    128: [5] * 64,
+    129: [9] + [5] * 63,
+    200: [13] * 8 + [9] * 56,
+}
+
+
+@pytest.mark.parametrize("n_groups", list(GROUP_COUNT_CASES))
+@pytest.mark.parametrize("M", [1, 4, 16])
+@pytest.mark.parametrize("sparse", ["gather", "mfma"])
+def test_exact_group_count_boundaries(gpu_lib, n_groups, M, sparse):
+    """Tiles whose group count sits on the boundaries of the per-lane group
+    loads (64 and 128 groups) give the exact result with both mappings and
+    both strip widths."""
+    if sparse == "gather" and M > 4:
+        pytest.skip("the gather mapping covers at most four rows")
+    counts = GROUP_COUNT_CASES[n_groups]
+    assert sum(-(-c // 4) for c in counts) == n_groups
+    prob = _column_pattern_problem(M, counts, seed=n_groups * 3 + M)
+    log(f"group-count boundary n_groups={n_groups} M={M} {sparse}")
+    y_ref = ref(prob).astype(np.float32)
+    flags = [0] if sparse == "gather" else [0, 16, 32]
+    for f in flags:
+        y = run(gpu_lib, prob, "fused", "f32", c_params(), 0, sparse, flags=f)
+        assert np.array_equal(y, y_ref), (n_groups, M, sparse, f)
+
+
 def test_exact_dense_only(gpu_lib):
     prob = make_exact_problem(16, 2048, 512, frac=0.02, seed=99)
     y32 = run(gpu_lib, prob, "dense", "f32")
