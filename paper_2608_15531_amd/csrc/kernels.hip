@@ -50,6 +50,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstddef>
 #include <type_traits>
 
 #include "device.hpp"
@@ -88,6 +89,10 @@ struct MatmulArgs {
   float* partials;
   uint32_t* counters;
 };
+
+static_assert(offsetof(MatmulArgs, X) + 8 <= 64 && offsetof(MatmulArgs, tile_indptr) == 64 &&
+                  offsetof(MatmulArgs, Y) >= 128 && sizeof(MatmulArgs) <= 192,
+              "argument lines: schedule and dense operands, sparse operands and LDS layout, output");
 
 // Global loads one tile costs in each mode (each counts once in vmcnt).
 template <int MB, int MODE, bool DENSE, bool SPARSE, int XR>
@@ -401,6 +406,13 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
   const int h = lane >> 4;                     // k-chunk of the MFMA operands
   const int c4 = lane & 15;                    // MFMA column / A row
 
+  // The arguments span three 64-byte scalar-cache lines.  One field of each is
+  // requested here, before anything waits on the first, so that a wave pays
+  // one memory round trip for all of them: otherwise the second line costs a
+  // round trip before the first tile's loads and the third one in the
+  // epilogue.
+  asm volatile("" ::"s"(args.G), "s"(args.tile_indptr), "s"(args.Y));
+
   // Work: the units (strip, tile) of each 32-row slab, strip-major
   // (u = strip * T + tile, which is also the Tile-COO tile index).  A
   // workgroup takes a contiguous range of units -- one (strip, K range) under
@@ -540,15 +552,22 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
         // `step` of lane (c4, h) is chunk 4 step + h of row c4 (rows past M
         // read row M-1, which is staged).  Both directions touch 16 distinct
         // 16-byte bank groups per 16 lanes.
+  // With one or two loads the chunks are stored already permuted to the
+        // operand order of the dequantised codes (XR permutes per tile instead
+        // of four); with four the count is the same either way, and permuting
+        // after the read keeps the stage store off the permutes' latency.
+        constexpr bool kPermuteOnStore = XR < 4;
   #pragma unroll
         for (int j = 0; j < XR; ++j)
-          *reinterpret_cast<uint4*>(xst + (4 * j + h) * 256 + ((c4 ^ (4 * j + h)) << 4)) = cur.x[j];
+          *reinterpret_cast<uint4*>(xst + (4 * j + h) * 256 + ((c4 ^ (4 * j + h)) << 4)) =
+              kPermuteOnStore ? permute_chunk(cur.x[j]) : cur.x[j];
         __builtin_amdgcn_wave_barrier();
         const int rr = min(c4, a.M - 1);
   #pragma unroll
-        for (int step = 0; step < 4; ++step)
-          A[0][step] = __builtin_bit_cast(bf16x8_t, permute_chunk(*reinterpret_cast<const uint4*>(
-                                                        xst + rr * 256 + (((4 * step + h) ^ rr) << 4))));
+        for (int step = 0; step < 4; ++step) {
+          const uint4 f = *reinterpret_cast<const uint4*>(xst + rr * 256 + (((4 * step + h) ^ rr) << 4));
+          A[0][step] = __builtin_bit_cast(bf16x8_t, kPermuteOnStore ? f : permute_chunk(f));
+        }
       } else {
   #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
