@@ -74,6 +74,20 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def warm_replays(torch, g, min_ms: float = 20.0, max_replays: int = 400):
+    """Replays graph g until the GPU has been busy for at least min_ms: after
+    host-side preparation (packing, captures) the first replays run slower
+    until the clocks ramp up, and one replay is not enough to absorb that."""
+    t0 = time.perf_counter()
+    for i in range(max_replays):
+        g.replay()
+        if i % 2 == 1:
+            torch.cuda.synchronize()
+            if (time.perf_counter() - t0) * 1e3 >= min_ms:
+                break
+    torch.cuda.synchronize()
+
+
 def kernel_source_digest():
     """sha256 over the device sources; counter figures are tied to it."""
     import hashlib
@@ -276,8 +290,7 @@ def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
         row = {"shape": c.name, "M": c.M}
         for vname, fn in variants.items():
             g = capture(lambda: [fn(c, i % R) for i in range(L)])
-            g.replay()
-            torch.cuda.synchronize()
+            warm_replays(torch, g)
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()
@@ -412,8 +425,7 @@ def sweep(fq, torch, which, dev, copies_min=4):
 
     def per_launch_us(fn, L, reps=4):
         g = capture(lambda: [fn(i) for i in range(L)])
-        g.replay()
-        torch.cuda.synchronize()
+        warm_replays(torch, g)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -681,8 +693,7 @@ def main():
 
     def per_launch_us(c, variant, reps):
         g = capture(lambda: [launch(c, i % R, variant) for i in range(LPG)])
-        g.replay()
-        torch.cuda.synchronize()
+        warm_replays(torch, g)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -720,8 +731,7 @@ def main():
                 x = torch.randn(d["M"], K, device=dev, dtype=torch.bfloat16)
                 out = torch.empty(d["M"], N, device=dev, dtype=torch.bfloat16)
                 g = capture(lambda: [torch.matmul(x, W, out=out) for W in Ws])
-                g.replay()
-                torch.cuda.synchronize()
+                warm_replays(torch, g)
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record()

@@ -1033,7 +1033,10 @@ int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
 //    LDS stage (measured at 9..16 rows).  With two 16-row blocks (17..32 rows) the per-tile work is
 //    heavier and covering every CU pays, unless the 32-column strips already
 //    give 192 workgroups of at most 32 tiles: 64-column strips split to at
-//    least 256 workgroups, four waves.
+//    least 256 workgroups, four waves -- or, where that overflows one
+//    workgroup per CU, half that split with eight waves (4096 x 6144 at 24
+//    and 32 rows: 13.5 and 14.6 us against 14.6 and 15.9 us for 32-column
+//    strips without a split).
 //  * Long K (down): 64-column strips split to about 512 workgroups, four
 //    waves; with two 16-row blocks (more than 16 rows) to about 256
 //    workgroups of eight waves (14336 x 4096 at 32 rows: 20.4 vs 21.9 us,
@@ -1046,9 +1049,12 @@ Shape default_shape(int T, int N, int n_slabs, int slab_M) {
   if (units64 >= 160) return {4, 0, 0};
   int S = 1;
   if (T <= 64) {
-    if (slab_M > 16 && (units32 < 192 || T > 32)) {
+    if (slab_M > 16) {
       while (units64 * S < 256 && 2 * S <= T / 8) S *= 2;
-      return {4, S, 4};
+      // four-wave workgroups would overflow one round on the CUs: half the
+      // split with eight waves, at least two tiles per wave
+      if (S >= 2 && units64 * S > 256 && T / (S / 2) >= 16) return {4, S / 2, 8};
+      if (units32 < 192 || T > 32) return {4, S, 4};
     }
     return {2, 1, T >= 8 ? 8 : 4};
   }

@@ -353,6 +353,10 @@ def test_debug_decode_rejects(lib):
     (1, 4096, 28672, dict(mapping="gather", x_stage_loads=0)),
     # long K: 64-column strips split to about 512 workgroups
     (4, 14336, 4096, dict(strip_cols=64, split_k=8, dense_waves=4, workgroups=512)),
+    # two 16-row blocks where four-wave workgroups would overflow one round:
+    # half that split, eight waves
+    (32, 4096, 6144, dict(strip_cols=64, split_k=2, dense_waves=8, workgroups=192)),
+    (24, 8192, 3072, dict(strip_cols=64, split_k=4, dense_waves=8, workgroups=192)),
     # long K with two 16-row blocks: about 256 workgroups of eight waves
     (32, 14336, 4096, dict(strip_cols=64, split_k=4, dense_waves=8, workgroups=256)),
     (64, 14336, 4096, dict(strip_cols=64, split_k=2, dense_waves=8, workgroups=256)),
