@@ -386,3 +386,49 @@ def test_launch_config_switches(lib):
         fq.fq_launch_config(1, 4096, 4096, group_mode=2)
     with pytest.raises(fq.FqError):
         fq.fq_launch_config(5, 4096, 4096, sparse="gather")
+
+
+def test_launch_plans_stay_within_kernel_limits(lib):
+    """Every launch the planner accepts, over a sweep of shapes, splits and
+    switches, fits the kernel's limits: at most 160 KB of LDS, at most 63
+    tiles per wave (one register of group offsets), a grid of strips x
+    splits x 32-row slabs, the gather mapping only at up to four rows on
+    64-column strips, and X staging exactly when one 16-row block uses the
+    MFMA mapping.  The default (no split, no switch) is accepted for every
+    shape."""
+    Ms = [1, 2, 3, 4, 5, 8, 9, 16, 17, 24, 32, 33, 48, 64, 100, 128]
+    Ks = [128, 256, 1024, 4096, 8192, 14336, 28672, 57344]
+    Ns = [64, 128, 192, 512, 4096, 6144, 14336, 28672, 57344]
+    switches = [0, fq.FQ_STRIP_32, fq.FQ_STRIP_64, fq.FQ_FOUR_WAVES, fq.FQ_SCHED_STREAM_K,
+                fq.FQ_SPARSE_WAVES, fq.FQ_STRIP_32 | fq.FQ_FOUR_WAVES]
+    accepted = 0
+    for M in Ms:
+        for K in Ks:
+            for N in Ns:
+                if K * N // 2 >= 1 << 31:
+                    continue
+                T = K // 128
+                for split_k in (0, 1, 2, 3, 7):
+                    for flags in switches:
+                        try:
+                            c = fq.fq_launch_config(M, K, N, split_k=split_k, flags=flags)
+                        except Exception:
+                            assert (split_k, flags) != (0, 0), (M, K, N)
+                            continue
+                        accepted += 1
+                        where = (M, K, N, split_k, flags, c)
+                        assert c["lds_bytes"] <= 160 * 1024, where
+                        assert c["dense_waves"] in (4, 8), where
+                        assert c["outlier_waves"] in (0, c["dense_waves"] // 2), where
+                        assert c["strip_cols"] in (32, 64), where
+                        if c["mapping"] == "gather":
+                            assert M <= 4 and c["strip_cols"] == 64, where
+                        stage = {1: 1, 2: 1, 3: 1, 4: 1, 5: 2, 8: 2}.get(M, 4 if M <= 16 else 0)
+                        assert c["x_stage_loads"] == (stage if c["mapping"] == "mfma" else 0), where
+                        if not c["stream_k"]:
+                            S = c["split_k"]
+                            assert 1 <= S <= T, where
+                            slabs = -(-M // 32)
+                            assert c["workgroups"] == N // c["strip_cols"] * S * slabs, where
+                            assert -(-(-(-T // S)) // c["dense_waves"]) <= 63, where
+    assert accepted > 10000
