@@ -157,7 +157,24 @@ def pmc_summary(fetch_csv, write_csv, sq_csv, log_path):
     write = sum(wd) / len(wd) * 1024 * wf
     alg = meta["algorithmic_bytes_per_launch"]
     cases = meta["pmc_pass"]
-    out = [f"Kernel `{kernel}`: launches {', '.join(cases)} of the Llama-3-8B decode step, "
+    out = ["# Fused W4A16 outlier matmul, dominant kernel: HBM traffic and SQ counters", "",
+           "Commands (repo root, MI355X, ROCm 7.2; `export TMPDIR=/tmp` first), one counter "
+           "pass each, then this summary (no GPU):", "",
+           "    timeout -s KILL 150 rocprofv3 --pmc FETCH_SIZE --output-format csv -d "
+           "gpurun_out/pmc_fetch -o run -- python3 -u bench.py --pmc-pass "
+           "> gpurun_out/pmc_fetch.log",
+           "    timeout -s KILL 150 rocprofv3 --pmc WRITE_SIZE --output-format csv -d "
+           "gpurun_out/pmc_write -o run -- python3 -u bench.py --pmc-pass",
+           "    timeout -s KILL 150 rocprofv3 --pmc SQ_WAVE_CYCLES SQ_BUSY_CYCLES "
+           "SQ_ACTIVE_INST_VALU SQ_VALU_MFMA_BUSY_CYCLES SQ_LDS_BANK_CONFLICT SQ_ACTIVE_INST_LDS "
+           "SQ_INSTS_VALU SQ_WAVES GRBM_GUI_ACTIVE --output-format csv -d gpurun_out/pmc_sq "
+           "-o run -- python3 -u bench.py --pmc-pass",
+           "    python bench.py --pmc-summary gpurun_out/pmc_fetch/run_counter_collection.csv "
+           "gpurun_out/pmc_write/run_counter_collection.csv "
+           "gpurun_out/pmc_sq/run_counter_collection.csv gpurun_out/pmc_fetch.log "
+           "> profiles/fused_llama3_8b_decode_traffic.md", "",
+           "(the .log file is the stdout of the first pass, which names the launches)", "",
+           f"Kernel `{kernel}`: launches {', '.join(cases)} of the Llama-3-8B decode step, "
            f"each once per rotated weight copy ({meta['copies']} copies), then one plain device "
            f"copy of {cal} bytes that calibrates the counters.", "",
            "## Calibration", "",
@@ -389,6 +406,153 @@ def pmc_summary_mfma(csv_path, log_path):
         fl = sum(d["MfmaFlopsBF16"] for d in ds) / len(ds)
         out.append(f"| {c['K']}x{c['N']} | {c['M']} | `{c['kernel']}` | {util:.1f} | {fl:.4g} | "
                    f"{c['flops']:.4g} |")
+    return out
+
+
+def _json_lines(path, prefix):
+    with open(path) as fh:
+        return [json.loads(line) for line in fh if line.startswith(prefix)]
+
+
+def trace_summary(stats_csv, traced_log, plain_log):
+    """Markdown summary of the rocprofv3 kernel trace of the default step
+    (stdout).  traced_log: stdout of the bench run under the profiler;
+    plain_log: stdout of a default bench run of the same tree.  No GPU."""
+    import csv
+    import paper_2608_15531_amd as fq
+    rows = list(csv.DictReader(open(stats_csv)))
+    traced = _json_lines(traced_log, '{"metric"')[0]
+    plain = _json_lines(plain_log, '{"metric"')[0]
+    inst = {}
+    for name, K, N in SHAPES:
+        for M in MS:
+            inst.setdefault(kernel_name(fq, M, K, N), []).append(f"{name}/M{M}")
+
+    def short(n):
+        return n.replace("void fqk::", "").split("(")[0].strip()
+
+    dom_name = traced["roofline"]["kernel"]
+    out = ["# Fused W4A16 outlier matmul, Llama-3-8B decode linears (M=1,4,8,16), "
+           "kernel-trace summary", "",
+           "Commands (repo root, MI355X, ROCm 7.2; `export TMPDIR=/tmp` first): the traced run, "
+           "a default run, then this summary (no GPU):", "",
+           "    rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_bench "
+           "-o bench -- python3 -u bench.py --steps 200 --warmup 20 --no-cpu-baseline "
+           "--no-compare > gpurun_out/prof_bench.log",
+           "    python3 -u bench.py > gpurun_out/bench_full.log",
+           "    python bench.py --trace-summary gpurun_out/prof_bench/bench_kernel_stats.csv "
+           "gpurun_out/prof_bench.log gpurun_out/bench_full.log "
+           "> profiles/fused_llama3_8b_decode_kernel_trace.md", "",
+           "Workload: qkv 4096x6144, o 4096x4096, gate_up 4096x28672, down 14336x4096 at "
+           "M=1,4,8,16; 1% uniform bf16 outliers, Tile-COO 128x64, 16 buckets, by-column groups "
+           "(the by-bucket step of the same run is included in the counts); 8 rotated weight "
+           "copies per shape (graph replay).", "",
+           "`matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR>`: MB 16-row blocks; "
+           "MODE 0 = LDS-gather outlier mapping, 1 = MFMA image mapping; NCB 16-column MFMA "
+           "blocks per strip (2: 32-column strips, 4: 64-column strips); NW waves per workgroup; "
+           "SK Stream-K; NWS extra outlier-only waves; XR row-wise X loads per tile reordered "
+           "through LDS (ceil(M/4); 0 = loads in operand order).", "",
+           f"Kernel sources sha256 (kernels.hip, device.hpp, internal.hpp): "
+           f"`{kernel_source_digest()}`", "",
+           "| kernel | launches (shapes, by-column step) | calls | total ns | average ns | min ns "
+           "| max ns |", "|---|---|---|---|---|---|---|"]
+    tc = tn = 0
+    for r in rows:
+        k = short(r["Name"])
+        if "matmul_kernel" in k:
+            tc += int(r["Calls"])
+            tn += int(r["TotalDurationNs"])
+        out.append(f"| `{k}` | {', '.join(inst.get(k, []))} | {r['Calls']} | "
+                   f"{r['TotalDurationNs']} | {float(r['AverageNs']):.0f} | {r['MinNs']} | "
+                   f"{r['MaxNs']} |")
+    dom = [r for r in rows if short(r["Name"]) == dom_name][0]
+    rt, rp = traced["roofline"], plain["roofline"]
+    if rp["traffic"]:
+        tail = f", traffic {rp['traffic']}."
+    else:
+        rec = measured_traffic(dom_name)
+        tail = (" (its roofline.traffic is null when the counter summary for these sources "
+                "was not yet committed")
+        if rec:
+            tail += (f"; with it committed, bench.py reports roofline.traffic "
+                     f"{rec['hbm_bytes_per_launch']} bytes per launch).")
+        else:
+            tail += ")."
+    out += ["", f"Dominant kernel `{dom_name}` ({', '.join(rt['launches'])}: the instance that "
+                f"moves most of the step's bytes): average {float(dom['AverageNs']) / 1e3:.2f} us "
+                f"per launch (kernel execution only).",
+            f"bench.py, same run: value {traced['value']} GB/s, ms_per_step "
+            f"{traced['ms_per_step']}; roofline.us_per_launch {rt['us_per_launch']} us (HIP events "
+            f"over warmed graph replays of each dominant matmul alone, 32 launches per graph, so "
+            f"it also holds the dispatch gap between consecutive kernels, about 1.3 us), achieved "
+            f"{rt['achieved']} GB/s, frac {rt['frac']}.",
+            f"The default bench run without the profiler (same tree): value {plain['value']} GB/s, "
+            f"ms_per_step {plain['ms_per_step']}, roofline.us_per_launch {rp['us_per_launch']} us, "
+            f"frac {rp['frac']}" + tail,
+            f"Every fused matmul launch of the run (warm-up replays included): {tc} calls, "
+            f"{tn / tc / 1e3:.2f} us on average."]
+    print("\n".join(out))
+
+
+def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
+    """Markdown summary of the three sweeps and the MFMA counter pass
+    (stdout).  No GPU."""
+    sw = {k: _json_lines(p, '{"sweep"') for k, p in
+          (("density", density_log), ("70b", b70_log), ("large-m", large_m_log))}
+    out = ["# Sweeps beyond the decode step: density and structure, Llama-3-70B decode "
+           "linears, larger M", "",
+           "Commands (repo root, MI355X, ROCm 7.2): one run per table (every launch is "
+           "graph-replayed over rotated weight copies, at least 4 and at least 1 GiB, warmed "
+           "for 20 ms, HIP events per launch), the MFMA counter pass "
+           "(`export TMPDIR=/tmp` first), then this summary (no GPU):", "",
+           "    python bench.py --sweep density > gpurun_out/sweep_density.log",
+           "    python bench.py --sweep 70b > gpurun_out/sweep_70b.log",
+           "    python bench.py --sweep large-m > gpurun_out/sweep_large-m.log",
+           "    timeout -s KILL 200 rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 --output-format csv "
+           "-d gpurun_out/pmc_mfma -o run -- python3 -u bench.py --pmc-pass-large-m "
+           "> gpurun_out/pmc_mfma.log",
+           "    python bench.py --sweep-summary gpurun_out/sweep_density.log "
+           "gpurun_out/sweep_70b.log gpurun_out/sweep_large-m.log "
+           "gpurun_out/pmc_mfma/run_counter_collection.csv gpurun_out/pmc_mfma.log "
+           "> profiles/sweeps_density_70b_large_m.md", "",
+           "Bytes are the algorithmic bytes of the operator (INT4 codes, fp16 scales, INT4 "
+           "zeros, stored Tile-COO bytes, X, Y); `% peak` is against 8 TB/s.  MFMA columns "
+           "(larger M): `alg TF` = (2MKN + 2M nnz) / t, `MFMA TF` = FLOPs the matrix cores "
+           "execute (dense, row-sum and outlier-image MFMAs, padded rows included) / t, against "
+           "the 2500 TFLOP/s dense bf16 peak.  Tile-COO: by-column groups, 16 buckets (the "
+           "library default).", "",
+           "## Density and structure (M=8, 4096x14336)", "",
+           "| outliers | clustered share | Tile-COO MB | fused us | GB/s | % peak | unfused us | "
+           "fused vs unfused | dense-only us | kernel |", "|---|---|---|---|---|---|---|---|---|---|"]
+    for r in sw["density"]:
+        out.append(f"| {100 * r['frac']:.1f}% {r['dist']} | {r.get('clustered_share', '-')} | "
+                   f"{r['tilecoo_bytes'] / 1e6:.2f} | {r['fused_us']:.2f} | {r['fused_GBs']:.0f} | "
+                   f"{r['pct_hbm_peak']} | {r['unfused_us']:.2f} | {r['fused_vs_unfused']:.2f}x | "
+                   f"{r['dense_only_us']:.2f} | `{r['kernel']}` |")
+    out += ["", "## Llama-3-70B decode linears (1% uniform)", "",
+            "| K x N | M | fused us | GB/s | % peak | unfused us | fused vs unfused | "
+            "dense-only us | kernel |", "|---|---|---|---|---|---|---|---|---|"]
+    for r in sw["70b"]:
+        out.append(f"| {r['K']}x{r['N']} | {r['M']} | {r['fused_us']:.2f} | {r['fused_GBs']:.0f} | "
+                   f"{r['pct_hbm_peak']} | {r['unfused_us']:.2f} | {r['fused_vs_unfused']:.2f}x | "
+                   f"{r['dense_only_us']:.2f} | `{r['kernel']}` |")
+    out += ["", "## Larger M (1% uniform)", "",
+            "| K x N | M | fused us | GB/s | % peak | alg TF | MFMA TF | MFMA % peak | unfused us "
+            "| fused vs unfused | dense-only us | kernel |",
+            "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in sw["large-m"]:
+        out.append(f"| {r['K']}x{r['N']} | {r['M']} | {r['fused_us']:.2f} | {r['fused_GBs']:.0f} | "
+                   f"{r['pct_hbm_peak']} | {r['alg_TFLOPs']} | {r['mfma_TFLOPs']} | "
+                   f"{r['mfma_util_pct']} | {r['unfused_us']:.2f} | {r['fused_vs_unfused']:.2f}x | "
+                   f"{r['dense_only_us']:.2f} | `{r['kernel']}` |")
+    out += ["", "## MFMA counters (larger M)", "",
+            "Four eager launches per case.  `MfmaUtil` is rocprofv3's derived metric (MFMA busy "
+            "cycles summed over SIMDs / (GPU-active cycles x SIMDs)); `MfmaFlopsBF16` counts 512 "
+            "x the bf16 MFMA math-op instructions.  The counted FLOPs equal the model that "
+            "`bench.py --sweep large-m` divides by time for its `MFMA TF` column.", ""]
+    out += pmc_summary_mfma(mfma_csv, mfma_log)
+    out += ["", "At 5 % clustered the requested outliers do not fit into the 2 % of columns (they "
+                "fill completely), so the realised clustered share is 40 %."]
     print("\n".join(out))
 
 
@@ -530,13 +694,26 @@ def main():
     ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "SQ_CSV", "LOG"),
                     help="no GPU: summarise the rocprofv3 counter CSVs of --pmc-pass runs "
                          "(SQ_CSV may be '-') into the traffic profile text")
+    ap.add_argument("--trace-summary", nargs=3, metavar=("STATS_CSV", "TRACED_LOG", "PLAIN_LOG"),
+                    help="no GPU: the kernel-trace profile text from rocprofv3's kernel stats "
+                         "and the bench output of the traced and of a plain run")
+    ap.add_argument("--sweep-summary", nargs=5,
+                    metavar=("DENSITY_LOG", "70B_LOG", "LARGE_M_LOG", "MFMA_CSV", "MFMA_LOG"),
+                    help="no GPU: the sweeps profile text from the three --sweep outputs and "
+                         "the --pmc-pass-large-m counter run")
     args = ap.parse_args()
+    if args.trace_summary:
+        trace_summary(*args.trace_summary)
+        return
+    if args.sweep_summary:
+        sweep_summary(*args.sweep_summary)
+        return
     if args.pmc_summary:
         fcsv, wcsv, sqcsv, logp = args.pmc_summary
         pmc_summary(fcsv, wcsv, None if sqcsv == "-" else sqcsv, logp)
         return
     if args.pmc_summary_mfma:
-        pmc_summary_mfma(*args.pmc_summary_mfma)
+        print("\n".join(pmc_summary_mfma(*args.pmc_summary_mfma)))
         return
 
     if args.gpus != 1:
