@@ -368,6 +368,22 @@ def test_full_size_sampled_columns(gpu_lib, shape, M, strip):
     assert rel <= F32_FROB
 
 
+@pytest.mark.parametrize("shape", FULL_SHAPES, ids=["qkv", "o", "gate_up", "down"])
+@pytest.mark.parametrize("M", [24, 32])
+def test_full_size_two_row_blocks_sampled_columns(gpu_lib, shape, M):
+    """The Llama-3-8B decode linears at 24 and 32 rows (two 16-row blocks) in
+    the default launch configuration (split-K with four or eight waves per
+    workgroup, depending on the shape), on sampled columns."""
+    K, N = shape
+    log(f"full two blocks K={K} N={N} M={M}")
+    prob = make_problem(M, K, N, frac=0.01, seed=seed_for(1, FULL_SHAPES.index(shape), 4 + M))
+    rng = np.random.default_rng(K + N + M)
+    cols = np.unique(np.concatenate([[0, 63, 64, N - 1], rng.choice(N, 128, replace=False)]))
+    y_ref = ref(prob, cols)
+    assert_bf16_close(run(gpu_lib, prob, "fused", "bf16")[:, cols], y_ref)
+    assert_f32_close(run(gpu_lib, prob, "fused", "f32")[:, cols], y_ref)
+
+
 # --------------------------------------- density sweep at its real shape --
 
 @pytest.mark.parametrize("frac", [0.0, 0.005, 0.01, 0.02, 0.05])
