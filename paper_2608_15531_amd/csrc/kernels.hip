@@ -386,11 +386,16 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
   for (int j = 0; j < 4; ++j) lds_store16(addr[j], 0u);
 }
 
+// Two 16-row blocks hold the most registers; they are kept to two waves per
+// SIMD (half the register file), which every instance launched fits without
+// spilling.
 template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS, int XR>
-__global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args) {
+__global__ void __launch_bounds__(64 * (NW + NWS))
+    __attribute__((amdgpu_waves_per_eu(MB == 2 ? 2 : 1))) matmul_kernel(MatmulArgs args) {
   static_assert(NCB == 4 || (NCB == 2 && MODE == 1), "32-column strips use the MFMA outlier mapping");
-  static_assert(XR == 0 || ((XR == 1 || XR == 2 || XR == 4) && MODE == 1 && MB == 1),
-                "X staging: 1, 2 or 4 row-wise loads, MFMA mapping, one 16-row block");
+  static_assert(XR == 0 || ((XR == 1 || XR == 2 || XR == 4) && MODE == 1 && MB == 1) ||
+                    ((XR == 6 || XR == 8) && MODE == 1 && MB == 2 && NWS == 0),
+                "X staging: 1, 2 or 4 row-wise loads for one 16-row block, 6 or 8 for two, MFMA mapping");
   // NWS > 0: warp specialisation (Sec. 3.1) -- NW dense waves and NWS outlier
   // waves share the strip's K range and the output reduction.
   constexpr int NT = NW + NWS;                 // waves per workgroup
@@ -502,10 +507,16 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
   }
   const uint32_t img = lds_address(bo);                  // this wave's image
   // X stage of this wave (4 XR rows x 256 bytes, 16-byte chunk q of row r at
-  // position q ^ r); its first 16 bytes double as the trash word, written by
-  // the scatter only between the stage's read and its next write
-  unsigned char* xst = smem + a.off_xs + size_t(wave) * (1024 * XR);
-  const uint32_t trash = lds_address(XR > 0 ? xst : smem + a.off_trash);
+  // position q ^ (r mod 16)).  With one 16-row block it has a place of its
+  // own, whose first 16 bytes double as the trash word, written by the
+  // scatter only between the stage's read and its next write.  With two
+  // blocks and an outlier image the stage (6 or 8 KB) lives in the image,
+  // which is all zero until the scatter: the stage is zeroed again once the
+  // X fragments are read, and the trash word has a place of its own.
+  constexpr bool kStageInImage = XR >= 6 && KS;
+  unsigned char* xst = kStageInImage ? reinterpret_cast<unsigned char*>(bo)
+                                     : smem + a.off_xs + size_t(wave) * (1024 * XR);
+  const uint32_t trash = lds_address((XR > 0 && !kStageInImage) ? xst : smem + a.off_trash);
 
 
   // The current segment (read by the lambdas below).
@@ -559,14 +570,25 @@ __global__ void __launch_bounds__(64 * (NW + NWS)) matmul_kernel(MatmulArgs args
         constexpr bool kPermuteOnStore = XR < 4;
   #pragma unroll
         for (int j = 0; j < XR; ++j)
-          *reinterpret_cast<uint4*>(xst + (4 * j + h) * 256 + ((c4 ^ (4 * j + h)) << 4)) =
+          *reinterpret_cast<uint4*>(xst + (4 * j + h) * 256 + ((c4 ^ ((4 * j + h) & 15)) << 4)) =
               kPermuteOnStore ? permute_chunk(cur.x[j]) : cur.x[j];
         __builtin_amdgcn_wave_barrier();
-        const int rr = min(c4, a.M - 1);
   #pragma unroll
-        for (int step = 0; step < 4; ++step) {
-          const uint4 f = *reinterpret_cast<const uint4*>(xst + rr * 256 + (((4 * step + h) ^ rr) << 4));
-          A[0][step] = __builtin_bit_cast(bf16x8_t, kPermuteOnStore ? f : permute_chunk(f));
+        for (int mb = 0; mb < MB; ++mb) {
+          const int rr = min(16 * mb + c4, a.M - 1);
+  #pragma unroll
+          for (int step = 0; step < 4; ++step) {
+            const uint4 f = *reinterpret_cast<const uint4*>(xst + rr * 256 +
+                                                             (((4 * step + h) ^ (rr & 15)) << 4));
+            A[mb][step] = __builtin_bit_cast(bf16x8_t, kPermuteOnStore ? f : permute_chunk(f));
+          }
+        }
+        if constexpr (kStageInImage) {
+          // give the image its zeros back (the LDS unit keeps a wave's
+          // accesses in order, so the reads above see the staged X)
+  #pragma unroll
+          for (int j = 0; j < XR; ++j)
+            *reinterpret_cast<uint4*>(xst + (4 * j + h) * 256 + (c4 << 4)) = uint4{0u, 0u, 0u, 0u};
         }
       } else {
   #pragma unroll
@@ -944,7 +966,7 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
 
 template <int MB, int MODE, int NCB, int NW, bool SK, int XR>
 int launch_roles(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
-  if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8)) {
+  if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8) && XR < 6) {
     if (dense && sparse && pl.NWS > 0)
       return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2, XR>(pl, a, s);
   }
@@ -959,6 +981,10 @@ int launch_sched(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool spar
     if (pl.XS == 4) return launch_roles<MB, MODE, NCB, NW, SK, 4>(pl, a, dense, sparse, s);
     if (pl.XS == 2) return launch_roles<MB, MODE, NCB, NW, SK, 2>(pl, a, dense, sparse, s);
     if (pl.XS == 1) return launch_roles<MB, MODE, NCB, NW, SK, 1>(pl, a, dense, sparse, s);
+  }
+  if constexpr (MODE == 1 && MB == 2 && !SK) {
+    if (pl.XS == 8) return launch_roles<MB, MODE, NCB, NW, SK, 8>(pl, a, dense, sparse, s);
+    if (pl.XS == 6) return launch_roles<MB, MODE, NCB, NW, SK, 6>(pl, a, dense, sparse, s);
   }
   return launch_roles<MB, MODE, NCB, NW, SK, 0>(pl, a, dense, sparse, s);
 }
@@ -1176,10 +1202,15 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   // reduction buffer (one tile per wave) reuses them
   const int n_slots = p.NWS > 0 ? p.NWS : p.NW;
   const size_t red_bytes = size_t(p.NW + p.NWS) * p.slab_M * (16 * p.NCB) * 4;
-  // X staging with the MFMA mapping and one 16-row block: ceil(M / 4)
-  // row-wise loads per tile (1, 2 or 4)
-  p.XS = (p.MODE == 1 && p.MB == 1) ? (p.slab_M <= 4 ? 1 : p.slab_M <= 8 ? 2 : 4) : 0;
-  if (p.XS) {
+  // X staging with the MFMA mapping: ceil(M / 4) row-wise loads per tile
+  // (1, 2 or 4) for one 16-row block, 6 or 8 for two (not beside outlier waves,
+  // whose dense waves have no image to stage in, nor under Stream-K, whose
+  // two-block kernels would spill registers)
+  p.XS = (p.MODE == 1 && p.MB == 1) ? (p.slab_M <= 4 ? 1 : p.slab_M <= 8 ? 2 : 4)
+         : (p.MODE == 1 && p.MB == 2 && p.NWS == 0 && !p.stream) ? (p.slab_M <= 24 ? 6 : 8) : 0;
+  // two blocks with an outlier image stage in the image: no LDS of their own
+  const bool stage_in_image = p.XS >= 6 && sparse;
+  if (p.XS && !stage_in_image) {
     // images, then an XS KB X stage per wave.  After the tile loop the
     // reduction buffer reuses them, and the split-K flag sits at the head of
     // wave 0's stage when the reduction buffer ends before it.  Each wave's
@@ -1200,7 +1231,7 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
     const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * p.slab_M * kTileN * 4 : 0;
     p.off_flag = align_up(p.off_shc + shc_bytes, 16);
     p.off_trash = p.off_flag + 16;
-    p.off_xs = p.off_trash;   // no X stages
+    p.off_xs = p.off_trash;   // no X stages of their own
     p.lds_bytes = p.off_trash + 16;
   }
   if (p.lds_bytes > 160 * 1024) return false;

@@ -28,7 +28,8 @@ CASES = [
     (16, 4096, 1024, 0, (), "auto"),            # four staged X loads
     (8, 14336, 256, 0, (), "auto"),             # long K: the planner splits
     (16, 2048, 512, 0, ("FQ_SCHED_STREAM_K",), "auto"),
-    (33, 1024, 256, 2, (), "auto"),             # two 32-row slabs, split-K
+    (33, 1024, 256, 2, (), "auto"),             # two 32-row slabs, split-K, eight staged loads
+    (20, 2048, 512, 0, (), "auto"),             # two 16-row blocks, six staged loads
     (5, 1024, 384, 2, ("FQ_STRIP_32",), "mfma"),
 ]
 

@@ -134,6 +134,8 @@ EXACT_CASES = [
     (64, 2048, 512, 0.01, 3, c_params()),
     (100, 1024, 192, 0.03, 0, c_params(group_mode=1, buckets_per_tile=8)),
     (128, 4096, 1024, 0.01, 0, c_params()),
+    # two 16-row blocks of at most 24 rows: six staged X loads
+    (20, 1024, 384, 0.02, 0, c_params()),
     # two 16-row blocks, half the split with eight waves (4096 x 6144-like)
     (24, 8192, 3072, 0.01, 0, c_params()),
     # long K with two 16-row blocks: split-K with eight waves per workgroup

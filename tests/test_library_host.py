@@ -345,7 +345,10 @@ def test_debug_decode_rejects(lib):
     (4, 4096, 6144, dict(x_stage_loads=1)),
     (5, 4096, 6144, dict(x_stage_loads=2)),
     (9, 4096, 6144, dict(x_stage_loads=4)),
-    (17, 4096, 6144, dict(x_staged=False, x_stage_loads=0)),
+    # two 16-row blocks: six or eight row-wise loads (the stage lives in the outlier image)
+    (17, 4096, 6144, dict(x_staged=True, x_stage_loads=6)),
+    (25, 4096, 6144, dict(x_staged=True, x_stage_loads=8)),
+    (128, 4096, 14336, dict(x_stage_loads=8)),
     # 160+ 64-column strips: 64-column strips, no split, eight waves
     (8, 4096, 14336, dict(strip_cols=64, split_k=1, dense_waves=8)),
     (1, 8192, 10240, dict(strip_cols=64, mapping="gather", x_staged=False)),
@@ -393,8 +396,9 @@ def test_launch_plans_stay_within_kernel_limits(lib):
     switches, fits the kernel's limits: at most 160 KB of LDS, at most 63
     tiles per wave (one register of group offsets), a grid of strips x
     splits x 32-row slabs, the gather mapping only at up to four rows on
-    64-column strips, and X staging exactly when one 16-row block uses the
-    MFMA mapping.  The default (no split, no switch) is accepted for every
+    64-column strips, and X staging exactly when the MFMA mapping is used
+    (one 16-row block, or two without outlier waves and
+    Stream-K).  The default (no split, no switch) is accepted for every
     shape."""
     Ms = [1, 2, 3, 4, 5, 8, 9, 16, 17, 24, 32, 33, 48, 64, 100, 128]
     Ks = [128, 256, 1024, 4096, 8192, 14336, 28672, 57344]
@@ -423,7 +427,10 @@ def test_launch_plans_stay_within_kernel_limits(lib):
                         assert c["strip_cols"] in (32, 64), where
                         if c["mapping"] == "gather":
                             assert M <= 4 and c["strip_cols"] == 64, where
-                        stage = {1: 1, 2: 1, 3: 1, 4: 1, 5: 2, 8: 2}.get(M, 4 if M <= 16 else 0)
+                        stage = {1: 1, 2: 1, 3: 1, 4: 1, 5: 2, 8: 2, 17: 6, 24: 6}.get(
+                            M, 4 if M <= 16 else 8)
+                        if M > 16 and (c["outlier_waves"] or c["stream_k"]):
+                            stage = 0   # two blocks stage only without outlier waves and Stream-K
                         assert c["x_stage_loads"] == (stage if c["mapping"] == "mfma" else 0), where
                         if not c["stream_k"]:
                             S = c["split_k"]
