@@ -15,9 +15,10 @@
 //             one 16-byte group per lane (the tiles of a strip are stored
 //             contiguously, so one load of tile_indptr gives every range).
 //             While tile t is computed, tile t+1 is in flight (Sec. 4.1).
-//             With the MFMA mapping and one 16-row block the X slice is loaded
-//             row-wise, 4 rows per load, and reordered through a per-wave LDS
-//             stage (template parameter XR = loads per tile).
+//             With the MFMA mapping the X slice is loaded row-wise, 4 rows
+//             per load, and reordered through a per-wave LDS stage (template
+//             parameter XR = loads per tile; with two 16-row blocks the stage
+//             lives in the wave's outlier image).
 //   dense     per 32-row step a lane turns 8 codes of each of its NCB columns
 //             into bf16 (128 + q) operands in registers and issues
 //             v_mfma_f32_16x16x32_bf16 against X; one more MFMA against an
@@ -1058,11 +1059,13 @@ int waves_per_workgroup(int T, int S, int n_strips, bool eight_waves) {
 //    the narrower strip.  This holds up to 16 rows, where X goes through the
 //    LDS stage (measured at 9..16 rows).  With two 16-row blocks (17..32 rows) the per-tile work is
 //    heavier and covering every CU pays, unless the 32-column strips already
-//    give 192 workgroups of at most 32 tiles: 64-column strips split to at
-//    least 256 workgroups, four waves -- or, where that overflows one
-//    workgroup per CU, half that split with eight waves (4096 x 6144 at 24
-//    and 32 rows: 13.5 and 14.6 us against 14.6 and 15.9 us for 32-column
-//    strips without a split).
+//    give 192 workgroups of at most 32 tiles: 64-column strips split to
+//    about 256 workgroups of eight waves (with X staged through the outlier
+//    image, 8192 x 8192 at 24 and 32 rows: 18.6 and 19.2 us against 21.2 and
+//    22.0 us with four waves), or, where that split overflows one workgroup
+//    per CU, half of it with eight waves (4096 x 6144 at 24 and 32 rows: 13.5
+//    and 14.6 us against 14.6 and 15.9 us for 32-column strips without a
+//    split).
 //  * Long K (down): 64-column strips split to about 512 workgroups, four
 //    waves; with two 16-row blocks (more than 16 rows) to about 256
 //    workgroups of eight waves (14336 x 4096 at 32 rows: 20.4 vs 21.9 us,
@@ -1080,7 +1083,8 @@ Shape default_shape(int T, int N, int n_slabs, int slab_M) {
       // four-wave workgroups would overflow one round on the CUs: half the
       // split with eight waves, at least two tiles per wave
       if (S >= 2 && units64 * S > 256 && T / (S / 2) >= 16) return {4, S / 2, 8};
-      if (units32 < 192 || T > 32) return {4, S, 4};
+      // at most one workgroup per CU: eight waves, so that two share each SIMD
+      if (units32 < 192 || T > 32) return {4, S, (units64 * S <= 256 && T / S >= 8) ? 8 : 4};
     }
     return {2, 1, T >= 8 ? 8 : 4};
   }

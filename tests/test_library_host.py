@@ -337,8 +337,9 @@ def test_debug_decode_rejects(lib):
     (8, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_stage_loads=2)),
     # few strips, up to 16 rows: 32-column strips, no split
     (16, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, workgroups=128)),
-    # few strips and two 16-row blocks: 64-column strips split to 256 workgroups, four waves
-    (32, 4096, 4096, dict(strip_cols=64, split_k=4, dense_waves=4, workgroups=256)),
+    # few strips and two 16-row blocks: 64-column strips split to 256 workgroups, eight waves
+    (32, 4096, 4096, dict(strip_cols=64, split_k=4, dense_waves=8, workgroups=256)),
+    (24, 8192, 8192, dict(strip_cols=64, split_k=2, dense_waves=8, workgroups=256)),
     # 32-column strips already give 192 workgroups of 32 tiles: no split
     (16, 4096, 6144, dict(strip_cols=32, split_k=1, dense_waves=8, x_stage_loads=4)),
     # X slices through the LDS stage with ceil(M/4) row-wise loads, one 16-row block
