@@ -494,6 +494,31 @@ def trace_summary(stats_csv, traced_log, plain_log):
     print("\n".join(out))
 
 
+def ablation_summary(log_path):
+    """Markdown summary of a --ablation run (stdout).  No GPU."""
+    rec = _json_lines(log_path, '{"ablation"')[0]
+    table = rec["per_matmul_us"]
+    names = [k for k in table[0] if k not in ("shape", "M")]
+    out = ["# Ablation of the fused kernel (Sec. 5.5 steps as this library implements them)", "",
+           "Commands (repo root, MI355X, ROCm 7.2), the run, then this summary (no GPU):", "",
+           "    python3 -u bench.py --ablation > gpurun_out/ablation.log",
+           "    python bench.py --ablation-summary gpurun_out/ablation.log "
+           "> profiles/ablation_llama3_8b_decode.md", "",
+           f"Workload: {rec['workload']}; Tile-COO 128x64, 16 buckets, by-column groups; "
+           "graph replays over rotated weight copies, warmed for 20 ms, HIP events per launch.  "
+           "unfused = dense W4A16 kernel then the Tile-COO SpMM kernel; SD = the fused kernel on "
+           "a Tile-COO packed without reordering; RE = with the column and element reordering "
+           "(the default packing); EW = extra outlier-only waves beside the dense waves "
+           "(`FQ_SPARSE_WAVES`); StreamK = the Stream-K schedule (`FQ_SCHED_STREAM_K`).", "",
+           "Geometric-mean speedup over the unfused baseline: " +
+           ", ".join(f"{k} {v:.3f}x" for k, v in rec["speedup"].items()) + ".", "",
+           "| shape | M | " + " | ".join(f"{n} us" for n in names) + " |",
+           "|---|---|" + "---|" * len(names)]
+    for t in table:
+        out.append(f"| {t['shape']} | {t['M']} | " + " | ".join(f"{t[n]:.2f}" for n in names) + " |")
+    print("\n".join(out))
+
+
 def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
     """Markdown summary of the three sweeps and the MFMA counter pass
     (stdout).  No GPU."""
@@ -697,6 +722,8 @@ def main():
     ap.add_argument("--trace-summary", nargs=3, metavar=("STATS_CSV", "TRACED_LOG", "PLAIN_LOG"),
                     help="no GPU: the kernel-trace profile text from rocprofv3's kernel stats "
                          "and the bench output of the traced and of a plain run")
+    ap.add_argument("--ablation-summary", metavar="LOG",
+                    help="no GPU: the ablation profile text from the output of --ablation")
     ap.add_argument("--sweep-summary", nargs=5,
                     metavar=("DENSITY_LOG", "70B_LOG", "LARGE_M_LOG", "MFMA_CSV", "MFMA_LOG"),
                     help="no GPU: the sweeps profile text from the three --sweep outputs and "
@@ -707,6 +734,9 @@ def main():
         return
     if args.sweep_summary:
         sweep_summary(*args.sweep_summary)
+        return
+    if args.ablation_summary:
+        ablation_summary(args.ablation_summary)
         return
     if args.pmc_summary:
         fcsv, wcsv, sqcsv, logp = args.pmc_summary
