@@ -304,7 +304,9 @@ fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes);
  *   cfg[7] dynamic LDS bytes per workgroup
  *   cfg[8] loads per tile of the X slice when it is loaded row-wise (4 rows per
  *          load) and reordered into MFMA operand order through LDS: 1, 2 or 4
- *          (ceil(M/4); the MFMA mapping with at most 16 rows), else 0
+ *          with at most 16 rows per 32-row slab (ceil(M/4)), 6 or 8 with 17..24
+ *          or 25..32 (not with outlier waves or Stream-K); the MFMA mapping
+ *          only, else 0
  * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_FORMAT (group_mode), FQ_ERR_UNSUPPORTED.
  */
 fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t group_mode,
