@@ -38,15 +38,24 @@ SHAPES = [("qkv", 4096, 6144), ("o", 4096, 4096), ("gate_up", 4096, 28672),
 MS = [1, 4, 8, 16]
 FRAC = 0.01
 COPY_CAL_BYTES = 256 << 20  # plain device copy used to calibrate FETCH_SIZE / WRITE_SIZE
-# Tile-COO packing of the tuned comparison step: by-bucket groups in one bucket
-# per tile (fewest padding slots)
-TUNED_TILECOO = {"group_mode": 1, "buckets_per_tile": 1}
+# The headline step uses the library's default Tile-COO packing (by-bucket
+# groups, one bucket per tile: the fewest padding slots).  The format of the
+# paper's decoding kernel (by-column groups, 16 buckets per tile) is timed
+# beside it.
+PAPER_TILECOO = {"group_mode": 0, "buckets_per_tile": 16}
+# streaming-read probe launch shapes (workgroups, waves per workgroup, 16-byte
+# loads in flight per lane); the fastest one at each byte count is the ceiling
+PROBE_CONFIGS = [(256, 8, 4), (512, 4, 4), (512, 8, 2), (1024, 4, 2), (1024, 4, 4),
+                 (2048, 4, 2)]
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fused_llama3_8b_decode_traffic.md")
 
 
-def kernel_name(fq, M, K, N):
-    """Template instance of the fused kernel the library launches for (M, K, N)."""
-    c = fq.fq_launch_config(M, K, N)
+def kernel_name(fq, M, K, N, packing=None):
+    """Template instance of the fused kernel the library launches for (M, K, N)
+    and a Tile-COO packed with `packing` (default: the library default)."""
+    packing = packing or {}
+    c = fq.fq_launch_config(M, K, N, buckets_per_tile=packing.get("buckets_per_tile"),
+                            group_mode=packing.get("group_mode"))
     mb = 1 if min(M, 32) <= 16 else 2
     mode = 0 if c["mapping"] == "gather" else 1
     sk = "true" if c["stream_k"] else "false"
@@ -86,6 +95,81 @@ def warm_replays(torch, g, min_ms: float = 20.0, max_replays: int = 400):
             if (time.perf_counter() - t0) * 1e3 >= min_ms:
                 break
     torch.cuda.synchronize()
+
+
+def capture_graph(torch, fn):
+    """A HIP graph of fn's launches (captured on a side stream after one
+    eager warm-up call)."""
+    g = torch.cuda.CUDAGraph()
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        fn()
+    torch.cuda.current_stream().wait_stream(st)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def graph_us(torch, g, launches, reps):
+    """Average duration per launch of a graph of `launches` launches, HIP
+    events around `reps` warmed replays on the replay stream."""
+    warm_replays(torch, g)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / (reps * launches)
+
+
+class StreamProbe:
+    """The streaming-read ceiling at a byte count: libfqprobe's plain 16-byte
+    read of the same number of bytes, over R rotated buffers (the rotation the
+    matmul's own measurement uses), graph-replayed like the matmuls; the
+    fastest of PROBE_CONFIGS."""
+
+    def __init__(self, torch, dev, R):
+        from paper_2608_15531_amd import probe
+        self.torch, self.dev, self.R, self.probe = torch, dev, R, probe
+        self.sink = torch.zeros(max(c[0] for c in PROBE_CONFIGS), dtype=torch.int32, device=dev)
+        self.cache = {}
+
+    def us(self, nbytes):
+        nbytes = -(-nbytes // 16) * 16
+        if nbytes in self.cache:
+            return self.cache[nbytes]
+        torch = self.torch
+        bufs = [torch.empty(nbytes // 4, dtype=torch.int32, device=self.dev)
+                for _ in range(self.R)]
+        L = 4 * self.R
+        best = None
+        for wgs, waves, d in PROBE_CONFIGS:
+            g = capture_graph(torch, lambda: [self.probe.fq_probe_stream_read(
+                bufs[i % self.R], nbytes, wgs, waves, d, self.sink) for i in range(L)])
+            t = graph_us(torch, g, L, max(2, 160 // L))
+            if best is None or t < best[0]:
+                best = (t, {"workgroups": wgs, "waves": waves, "loads_in_flight": d})
+            del g
+        del bufs
+        self.cache[nbytes] = best
+        return best
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def kernel_source_digest():
@@ -224,36 +308,80 @@ def pmc_summary(fetch_csv, write_csv, sq_csv, log_path):
     print("\n".join(out))
 
 
-def cpu_baseline(tilecoo_bytes: dict, budget_s: float = 20.0):
-    """Time the fp64 oracle (as it stands) on the host on a bounded sample of
-    the step: the M=1 matmuls, smallest first, until the budget is spent."""
+def cpu_baseline(fq, col_fraction: float = 0.25, runs: int = 3):
+    """The fp64 NumPy oracle as it stands, timed on the host cores this
+    process may use (BLAS threads pinned to that count), wall-clock median of
+    `runs` runs per case, on a bounded sample of the workloads: the small
+    single matmul (4096 x 4096) at M = 1, 4, 8, 16, and the four Llama-3-8B
+    decode linears at M = 1, each on its first `col_fraction` of the columns
+    (a contiguous block; bytes counted for that block).  Also the oracle's
+    own Tile-COO pack against the library's fq_pack_tile_coo on the 4096 x
+    4096 outliers, same packing.  Tile-COO bytes are the library default
+    packing's, as in the step."""
     import oracle
     from synth import make_problem, seed_for
+    cores = len(os.sched_getaffinity(0))
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)
     except Exception:  # pragma: no cover
-        threads = 1
-    done, t_total, b_total = [], 0.0, 0
-    order = sorted(range(len(SHAPES)), key=lambda i: SHAPES[i][1] * SHAPES[i][2])
-    for si in order:
-        name, K, N = SHAPES[si]
+        limiter = None
+
+    def median_s(fn):
+        ts = []
+        for _ in range(runs):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return float(np.median(ts))
+
+    rows, t_total, b_total = [], 0.0, 0
+    # the small single matmul at every row count of the decode sweep
+    for mi, M in enumerate(MS):
+        p = make_problem(M, 4096, 4096, frac=FRAC, seed=seed_for(0, 0, mi))
+        host = fq.fq_pack_tile_coo(4096, 4096, p.k, p.n, p.v)
+        nb = algorithmic_bytes(M, 4096, 4096, int(host.sizes.bytes))
+        oracle.matmul(p.X, p.Wq, p.scales, p.zeros, 4096, 4096, 128, p.k, p.n, p.v)   # warm
+        t = median_s(lambda: oracle.matmul(p.X, p.Wq, p.scales, p.zeros, 4096, 4096, 128,
+                                           p.k, p.n, p.v))
+        rows.append({"case": f"4096x4096 M={M}", "s": round(t, 3), "bytes": nb})
+        t_total += t
+        b_total += nb
+    # the decode linears at M = 1, a contiguous block of columns each
+    for si, (name, K, N) in enumerate(SHAPES):
         p = make_problem(1, K, N, frac=FRAC, seed=seed_for(1, si, 0))
-        t0 = time.perf_counter()
-        oracle.matmul(p.X, p.Wq, p.scales, p.zeros, K, N, 128, p.k, p.n, p.v)
-        t_total += time.perf_counter() - t0
-        b_total += algorithmic_bytes(1, K, N, tilecoo_bytes[name])
-        done.append(f"{name}(M=1)")
-        if t_total > budget_s:
-            break
-    return {"value": round(b_total / t_total / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"fp64 NumPy oracle on {', '.join(done)} of the step, one run each, "
-                      f"{t_total:.1f} s of CPU time; GB/s counts the same algorithmic bytes"}
+        host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v)
+        ncols = max(64, int(N * col_fraction) // 64 * 64)
+        cols = np.arange(ncols)
+        nb = int(round(algorithmic_bytes(1, K, N, int(host.sizes.bytes)) * ncols / N))
+        t = median_s(lambda: oracle.matmul(p.X, p.Wq, p.scales, p.zeros, K, N, 128, p.k, p.n,
+                                           p.v, cols))
+        rows.append({"case": f"{name} {K}x{N} M=1 columns [0,{ncols})", "s": round(t, 3),
+                     "bytes": nb})
+        t_total += t
+        b_total += nb
+    # Tile-COO pack: the oracle's against the library's, same outliers and packing
+    p = make_problem(1, 4096, 4096, frac=FRAC, seed=seed_for(0, 0, 0))
+    d = fq.fq_default_tilecoo_params()
+    op = oracle.Params(buckets=d.buckets_per_tile, group_mode=d.group_mode, reorder=d.reorder)
+    pack_oracle = median_s(lambda: oracle.pack_tile_coo(4096, 4096, p.k, p.n, p.v, op))
+    pack_lib = median_s(lambda: fq.fq_pack_tile_coo(4096, 4096, p.k, p.n, p.v))
+    if limiter is not None:
+        limiter.restore_original_limits()
+    return {"value": round(b_total / t_total / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "sample": f"fp64 NumPy oracle, median of {runs} wall-clock runs each, BLAS threads "
+                      f"pinned to the {cores} cores of os.sched_getaffinity: 4096x4096 at "
+                      f"M=1,4,8,16 and the Llama-3-8B decode linears at M=1 on their first "
+                      f"{col_fraction:.0%} of columns; {t_total:.1f} s of medians over "
+                      f"{b_total / 1e6:.1f} MB of algorithmic bytes",
+            "per_case": rows,
+            "pack_4096x4096_s": {"oracle_pack_tile_coo": round(pack_oracle, 3),
+                                 "library_fq_pack_tile_coo": round(pack_lib, 4)}}
 
 
 def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
-    """Per-matmul graph-replay times of the paper's ablation steps (Sec. 5.5)
+    """Per-matmul graph-replay times of the paper's ablation steps (Sec. 5.4)
     as this library implements them: the unfused two-kernel baseline; SD, the
     fused kernel on an unreordered Tile-COO; SD+RE, with the column and element
     reordering of Sec. 3.2.2 (the default configuration); SD+EW and SD+EW+RE,
@@ -261,12 +389,13 @@ def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
     workgroup (warp specialisation, FQ_SPARSE_WAVES); and the default with
     the Stream-K schedule.  Prints one JSON line."""
     from synth import make_problem, seed_for
-    # Tile-COO without reordering, one per shape, R copies
+    # The paper's format (by-column groups, 16 buckets per tile), where the
+    # reordering has buckets to balance: without reordering, one per shape,
+    # R copies; the reordered one is each case's tcs_paper.
     plain = {}
     for si, (name, K, N) in enumerate(SHAPES):
         p = make_problem(1, K, N, frac=FRAC, seed=seed_for(1, si, 0))
-        prm = fq.fq_default_tilecoo_params()
-        prm.reorder = 0
+        prm = dict(PAPER_TILECOO, reorder=0)
         host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v, prm)
         plain[name] = [fq.TileCOODevice(host, dev) for _ in range(R)]
     need_sk = max(fq.fq_workspace_bytes(c.M, c.K, c.N, flags=fq.FQ_SCHED_STREAM_K) for c in cases)
@@ -275,17 +404,19 @@ def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
     EW = fq.FQ_SPARSE_WAVES
     variants = {
         "unfused": lambda c, r: fq.fq_w4a16_outlier_matmul_unfused(
-            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws),
+            c.X, *c.weights[r], c.tcs_paper[r], Y=c.Y, ws=ws),
         "SD": lambda c, r: fq.fq_w4a16_outlier_matmul(
             c.X, *c.weights[r], plain[c.name][r], Y=c.Y, ws=ws),
         "SD+RE": lambda c, r: fq.fq_w4a16_outlier_matmul(
-            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws),
+            c.X, *c.weights[r], c.tcs_paper[r], Y=c.Y, ws=ws),
         "SD+EW": lambda c, r: fq.fq_w4a16_outlier_matmul(
             c.X, *c.weights[r], plain[c.name][r], Y=c.Y, ws=ws_big, flags=EW),
         "SD+EW+RE": lambda c, r: fq.fq_w4a16_outlier_matmul(
-            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws_big, flags=EW),
+            c.X, *c.weights[r], c.tcs_paper[r], Y=c.Y, ws=ws_big, flags=EW),
         "SD+RE+StreamK": lambda c, r: fq.fq_w4a16_outlier_matmul(
-            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws_big, flags=fq.FQ_SCHED_STREAM_K),
+            c.X, *c.weights[r], c.tcs_paper[r], Y=c.Y, ws=ws_big, flags=fq.FQ_SCHED_STREAM_K),
+        "default": lambda c, r: fq.fq_w4a16_outlier_matmul(
+            c.X, *c.weights[r], c.tcs[r], Y=c.Y, ws=ws),
     }
 
     def capture(fn):
@@ -325,7 +456,10 @@ def ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None):
         r = np.array([t["unfused"] / t[vname] for t in table])
         geo[vname] = round(float(np.exp(np.log(r).mean())), 4)
     print(json.dumps({"ablation": "geometric-mean speedup over the unfused two-kernel baseline",
-                      "workload": "Llama-3-8B decode linears at M=1,4,8,16, 1% uniform outliers",
+                      "workload": "Llama-3-8B decode linears at M=1,4,8,16, 1% uniform outliers; "
+                                  "Tile-COO in the paper's format (by-column groups, 16 buckets "
+                                  "per tile) except 'default' (the library default packing: "
+                                  "by-bucket groups, one bucket per tile)",
                       "speedup": geo, "per_matmul_us": table}), flush=True)
 
 
@@ -444,8 +578,9 @@ def trace_summary(stats_csv, traced_log, plain_log):
            "gpurun_out/prof_bench.log gpurun_out/bench_full.log "
            "> profiles/fused_llama3_8b_decode_kernel_trace.md", "",
            "Workload: qkv 4096x6144, o 4096x4096, gate_up 4096x28672, down 14336x4096 at "
-           "M=1,4,8,16; 1% uniform bf16 outliers, Tile-COO 128x64, 16 buckets, by-column groups "
-           "(the by-bucket step of the same run is included in the counts); 8 rotated weight "
+           "M=1,4,8,16; 1% uniform bf16 outliers, Tile-COO 128x64, the library default packing "
+           "(by-bucket groups, one bucket per tile; the paper-format step of the same run, "
+           "by-column groups with 16 buckets, is included in the counts); 8 rotated weight "
            "copies per shape (graph replay).", "",
            "`matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR>`: MB 16-row blocks; "
            "MODE 0 = LDS-gather outlier mapping, 1 = MFMA image mapping; NCB 16-column MFMA "
@@ -454,7 +589,7 @@ def trace_summary(stats_csv, traced_log, plain_log):
            "through LDS (ceil(M/4); 0 = loads in operand order).", "",
            f"Kernel sources sha256 (kernels.hip, device.hpp, internal.hpp): "
            f"`{kernel_source_digest()}`", "",
-           "| kernel | launches (shapes, by-column step) | calls | total ns | average ns | min ns "
+           "| kernel | launches (shapes, default packing) | calls | total ns | average ns | min ns "
            "| max ns |", "|---|---|---|---|---|---|---|"]
     tc = tn = 0
     for r in rows:
@@ -499,12 +634,12 @@ def ablation_summary(log_path):
     rec = _json_lines(log_path, '{"ablation"')[0]
     table = rec["per_matmul_us"]
     names = [k for k in table[0] if k not in ("shape", "M")]
-    out = ["# Ablation of the fused kernel (Sec. 5.5 steps as this library implements them)", "",
+    out = ["# Ablation of the fused kernel (Sec. 5.4 steps as this library implements them)", "",
            "Commands (repo root, MI355X, ROCm 7.2), the run, then this summary (no GPU):", "",
            "    python3 -u bench.py --ablation > gpurun_out/ablation.log",
            "    python bench.py --ablation-summary gpurun_out/ablation.log "
            "> profiles/ablation_llama3_8b_decode.md", "",
-           f"Workload: {rec['workload']}; Tile-COO 128x64, 16 buckets, by-column groups; "
+           f"Workload: {rec['workload']}; Tile-COO 128x64; "
            "graph replays over rotated weight copies, warmed for 20 ms, HIP events per launch.  "
            "unfused = dense W4A16 kernel then the Tile-COO SpMM kernel; SD = the fused kernel on "
            "a Tile-COO packed without reordering; RE = with the column and element reordering "
@@ -544,8 +679,8 @@ def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
            "zeros, stored Tile-COO bytes, X, Y); `% peak` is against 8 TB/s.  MFMA columns "
            "(larger M): `alg TF` = (2MKN + 2M nnz) / t, `MFMA TF` = FLOPs the matrix cores "
            "execute (dense, row-sum and outlier-image MFMAs, padded rows included) / t, against "
-           "the 2500 TFLOP/s dense bf16 peak.  Tile-COO: by-column groups, 16 buckets (the "
-           "library default).", "",
+           "the 2500 TFLOP/s dense bf16 peak.  Tile-COO: the library default packing (by-bucket "
+           "groups, one bucket per tile).", "",
            "## Density and structure (M=8, 4096x14336)", "",
            "| outliers | clustered share | Tile-COO MB | fused us | GB/s | % peak | unfused us | "
            "fused vs unfused | dense-only us | kernel |", "|---|---|---|---|---|---|---|---|---|---|"]
@@ -561,6 +696,17 @@ def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
         out.append(f"| {r['K']}x{r['N']} | {r['M']} | {r['fused_us']:.2f} | {r['fused_GBs']:.0f} | "
                    f"{r['pct_hbm_peak']} | {r['unfused_us']:.2f} | {r['fused_vs_unfused']:.2f}x | "
                    f"{r['dense_only_us']:.2f} | `{r['kernel']}` |")
+    out += ["", "Layer aggregate (the four Llama-3-70B linears of one decode layer: total "
+                "algorithmic bytes / total fused time):", "",
+            "| M | bytes | fused us | GB/s | % peak | unfused us | fused vs unfused |",
+            "|---|---|---|---|---|---|---|"]
+    for M in sorted({r["M"] for r in sw["70b"]}):
+        rs = [r for r in sw["70b"] if r["M"] == M]
+        b = sum(r["bytes"] for r in rs)
+        t = sum(r["fused_us"] for r in rs)
+        tu = sum(r["unfused_us"] for r in rs)
+        out.append(f"| {M} | {b} | {t:.2f} | {b / t / 1e3:.0f} | "
+                   f"{100 * b / t / 1e3 / HBM_PEAK_GBS:.1f} | {tu:.2f} | {tu / t:.2f}x |")
     out += ["", "## Larger M (1% uniform)", "",
             "| K x N | M | fused us | GB/s | % peak | alg TF | MFMA TF | MFMA % peak | unfused us "
             "| fused vs unfused | dense-only us | kernel |",
@@ -672,18 +818,130 @@ def sweep(fq, torch, which, dev, copies_min=4):
             print(json.dumps(rec), flush=True)
 
 
+TRACE_WARM, TRACE_REPS = 2, 6   # replays per case in the kernel-trace pass
+
+
+def trace_pass(fq, torch, order, launch, R, dev):
+    """For a rocprofv3 --kernel-trace run: each (shape, M) fused matmul alone,
+    a graph of 4R launches over the rotated copies replayed a fixed number of
+    times, in step order; then the bf16 GEMM comparator (torch.matmul on
+    hipBLASLt) of each shape at M = 1 and 16.  One JSON line names the
+    sequence, so the trace splits per matmul (--trace-per-matmul)."""
+    torch.backends.cuda.preferred_blas_library("cublaslt")
+    L = 4 * R
+    seq = []
+    for c in order:
+        g = capture_graph(torch, lambda c=c: [launch(c, i % R, "fused") for i in range(L)])
+        for _ in range(TRACE_WARM + TRACE_REPS):
+            g.replay()
+        torch.cuda.synchronize()
+        seq.append({"case": f"{c.name}/M{c.M}", "kernel": kernel_name(fq, c.M, c.K, c.N),
+                    "bytes": c.bytes, "launches": L * (1 + TRACE_WARM + TRACE_REPS),
+                    "untimed": L * (1 + TRACE_WARM)})
+        del g
+    gemm = []
+    for name, K, N in SHAPES:
+        W = torch.randn(K, N, device=dev, dtype=torch.bfloat16)
+        for M in (1, 16):
+            x = torch.randn(M, K, device=dev, dtype=torch.bfloat16)
+            out = torch.empty(M, N, device=dev, dtype=torch.bfloat16)
+            torch.cuda.synchronize()
+            for _ in range(8):
+                torch.matmul(x, W, out=out)
+            torch.cuda.synchronize()
+            gemm.append(f"{name}/M{M}")
+        del W
+    print(json.dumps({"trace_pass": seq, "gemm": gemm,
+                      "blas": str(torch.backends.cuda.preferred_blas_library())}), flush=True)
+
+
+def trace_per_matmul(trace_csv, log_path):
+    """Markdown on stdout: rocprofv3 kernel-only durations of a --trace-pass
+    run split per (shape, M), and the bf16 GEMM comparator's kernel names.
+    The pass launches each case's graph (1 capture warm-up call plus
+    TRACE_WARM + TRACE_REPS replays of 4R launches) in order, so the fused
+    dispatches, sorted by start time, split into consecutive runs.  No GPU."""
+    import csv
+    meta = _json_lines(log_path, '{"trace_pass"')[0]
+    rows = list(csv.DictReader(open(trace_csv)))
+    fused = sorted((r for r in rows if "matmul_kernel" in r["Kernel_Name"]),
+                   key=lambda r: int(r["Start_Timestamp"]))
+    need = sum(c["launches"] for c in meta["trace_pass"])
+    if len(fused) != need:
+        raise SystemExit(f"{len(fused)} fused dispatches in the trace, expected {need}")
+
+    def short(n):
+        return n.replace("void fqk::", "").split("(")[0].strip()
+    out_rows, inst = [], {}
+    i = 0
+    for c in meta["trace_pass"]:
+        chunk = fused[i:i + c["launches"]]
+        i += c["launches"]
+        names = {short(r["Kernel_Name"]) for r in chunk}
+        if names != {c["kernel"]}:
+            raise SystemExit(f"{c['case']}: kernels {names}, expected {c['kernel']}")
+        ns = np.array([int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+                       for r in chunk[c["untimed"]:]], dtype=np.float64)
+        med, mean = float(np.median(ns)) / 1e3, float(ns.mean()) / 1e3
+        out_rows.append((c, med, mean, ns.size))
+        inst.setdefault(c["kernel"], []).append((c, mean, ns.size))
+    out = ["# Fused W4A16 outlier matmul, per-matmul kernel-only durations (rocprofv3 kernel "
+           "trace), Llama-3-8B decode linears", "",
+           "Commands (repo root, MI355X, ROCm 7.2; `export TMPDIR=/tmp` first), then this "
+           "summary (no GPU):", "",
+           "    rocprofv3 --kernel-trace --output-format csv -d gpurun_out/trace_pm -o run -- "
+           "python3 -u bench.py --trace-pass > gpurun_out/trace_pm.log",
+           "    python bench.py --trace-per-matmul gpurun_out/trace_pm/run_kernel_trace.csv "
+           "gpurun_out/trace_pm.log > profiles/fused_llama3_8b_decode_per_matmul.md", "",
+           f"Each case: a graph of {meta['trace_pass'][0]['launches'] // (1 + TRACE_WARM + TRACE_REPS)}"
+           f" launches cycling over the rotated weight copies, {TRACE_REPS} timed replays after "
+           f"{TRACE_WARM} warm-up replays and the capture's warm-up call (not counted).  "
+           "Tile-COO: the library default packing (by-bucket groups, one bucket per tile).  "
+           "`frac` = algorithmic bytes / median kernel duration / 8 TB/s.", "",
+           f"Kernel sources sha256 (kernels.hip, device.hpp, internal.hpp): "
+           f"`{kernel_source_digest()}`", "",
+           "| matmul | kernel | launches | median us | mean us | bytes | GB/s (median) | frac |",
+           "|---|---|---|---|---|---|---|---|"]
+    for c, med, mean, n in out_rows:
+        out.append(f"| {c['case']} | `{c['kernel']}` | {n} | {med:.3f} | {mean:.3f} | "
+                   f"{c['bytes']} | {c['bytes'] / med / 1e3:.0f} | "
+                   f"{c['bytes'] / med / 1e3 / HBM_PEAK_GBS:.3f} |")
+    out += ["", "Per kernel instance (launch-weighted averages over its matmuls):", "",
+            "| kernel | matmuls | mean us per launch | mean bytes per launch | frac |",
+            "|---|---|---|---|---|"]
+    for k, lst in inst.items():
+        n = sum(x[2] for x in lst)
+        t = sum(x[1] * x[2] for x in lst) / n
+        b = sum(x[0]["bytes"] * x[2] for x in lst) / n
+        out.append(f"| `{k}` | {', '.join(x[0]['case'] for x in lst)} | {t:.3f} | {b:.0f} | "
+                   f"{b / t / 1e3 / HBM_PEAK_GBS:.3f} |")
+    last_fused = int(fused[-1]["End_Timestamp"])
+    gk = {}
+    for r in rows:
+        if int(r["Start_Timestamp"]) > last_fused and "matmul_kernel" not in r["Kernel_Name"]:
+            k = r["Kernel_Name"].split("(")[0][:120]
+            gk.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    out += ["", f"bf16 GEMM comparator (torch.matmul, preferred BLAS {meta['blas']}; cases "
+                f"{', '.join(meta['gemm'])}, 8 eager calls each, randn operands): kernels "
+                "launched after the fused matmuls:", "",
+            "| kernel | dispatches | mean us |", "|---|---|---|"]
+    for k, v in sorted(gk.items(), key=lambda kv: -len(kv[1])):
+        out.append(f"| `{k}` | {len(v)} | {np.mean(v) / 1e3:.2f} |")
+    print("\n".join(out))
+
+
 class Case:
     """One (shape, M) matmul with R rotated weight copies on the device."""
 
-    def __init__(self, fq, torch, name, K, N, M, weights, tcs, x, dev, tcs_bucket=None):
+    def __init__(self, fq, torch, name, K, N, M, weights, tcs, x, dev, tcs_paper=None):
         self.name, self.K, self.N, self.M = name, K, N, M
         self.weights = weights            # list of (Wq, scales, zeros)
-        self.tcs = tcs                    # list of TileCOODevice (by-column groups)
-        self.tcs_bucket = tcs_bucket      # the same outliers with by-bucket groups
+        self.tcs = tcs                    # list of TileCOODevice (library default packing)
+        self.tcs_paper = tcs_paper        # the same outliers in the paper's format
         self.X = x
         self.Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
         self.bytes = algorithmic_bytes(M, K, N, tcs[0].nbytes)
-        self.bytes_bucket = algorithmic_bytes(M, K, N, tcs_bucket[0].nbytes) if tcs_bucket else None
+        self.bytes_paper = algorithmic_bytes(M, K, N, tcs_paper[0].nbytes) if tcs_paper else None
 
 
 def main():
@@ -724,11 +982,21 @@ def main():
                          "and the bench output of the traced and of a plain run")
     ap.add_argument("--ablation-summary", metavar="LOG",
                     help="no GPU: the ablation profile text from the output of --ablation")
+    ap.add_argument("--trace-pass", action="store_true",
+                    help="no timing: each matmul's fused graph replayed a fixed number of "
+                         "times, then the bf16 GEMM comparator, for a rocprofv3 --kernel-trace "
+                         "run split per matmul by --trace-per-matmul")
+    ap.add_argument("--trace-per-matmul", nargs=2, metavar=("KERNEL_TRACE_CSV", "LOG"),
+                    help="no GPU: per-matmul kernel-only durations from a --trace-pass run's "
+                         "kernel trace")
     ap.add_argument("--sweep-summary", nargs=5,
                     metavar=("DENSITY_LOG", "70B_LOG", "LARGE_M_LOG", "MFMA_CSV", "MFMA_LOG"),
                     help="no GPU: the sweeps profile text from the three --sweep outputs and "
                          "the --pmc-pass-large-m counter run")
     args = ap.parse_args()
+    if args.trace_per_matmul:
+        trace_per_matmul(*args.trace_per_matmul)
+        return
     if args.trace_summary:
         trace_summary(*args.trace_summary)
         return
@@ -768,28 +1036,31 @@ def main():
         return
 
     # ---------------------------------------------------------- inputs
+    # torch.matmul, the bf16 GEMM comparator, on hipBLASLt (torch's "cublaslt"
+    # backend on ROCm); the backend torch reports is recorded with the results
+    torch.backends.cuda.preferred_blas_library("cublaslt")
+    blas = str(torch.backends.cuda.preferred_blas_library())
     cases = []
     pack_s = {}
-    tilecoo_bytes = {}
     for si, (name, K, N) in enumerate(SHAPES):
         t0 = time.perf_counter()
         p = make_problem(1, K, N, frac=FRAC, seed=seed_for(1, si, 0))
         t1 = time.perf_counter()
         host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v)
         pack_s[name] = time.perf_counter() - t1
-        tilecoo_bytes[name] = int(host.sizes.bytes)
-        host_b = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v, TUNED_TILECOO)
-        weights, tcs, tcs_b = [], [], []
+        host_p = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v, PAPER_TILECOO)
+        weights, tcs, tcs_p = [], [], []
         for _ in range(R):
             weights.append(fq.to_device(p, dev)[1:])
             tcs.append(fq.TileCOODevice(host, dev))
-            tcs_b.append(fq.TileCOODevice(host_b, dev))
+            tcs_p.append(fq.TileCOODevice(host_p, dev))
         log(f"[setup] {name} K={K} N={N}: generate {t1 - t0:.1f}s, pack {pack_s[name]:.2f}s, "
-            f"tilecoo {host.sizes.bytes / 1e6:.2f} MB, {R} copies")
+            f"tilecoo {host.sizes.bytes / 1e6:.2f} MB (paper format "
+            f"{host_p.sizes.bytes / 1e6:.2f} MB), {R} copies")
         for mi, M in enumerate(MS):
             xb = make_activations(M, K, seed_for(1, si, mi))
             x = torch.from_numpy(xb.view(np.int16).copy()).view(torch.bfloat16).to(dev)
-            cases.append(Case(fq, torch, name, K, N, M, weights, tcs, x, dev, tcs_b))
+            cases.append(Case(fq, torch, name, K, N, M, weights, tcs, x, dev, tcs_p))
         del p
     order = sorted(cases, key=lambda c: (c.M, [s[0] for s in SHAPES].index(c.name)))
     step_bytes = sum(c.bytes for c in order)
@@ -802,8 +1073,8 @@ def main():
         Wq, s, z = c.weights[r]
         if variant == "fused":
             fq.fq_w4a16_outlier_matmul(c.X, Wq, s, z, c.tcs[r], Y=c.Y, ws=ws)
-        elif variant == "fused_bucket":
-            fq.fq_w4a16_outlier_matmul(c.X, Wq, s, z, c.tcs_bucket[r], Y=c.Y, ws=ws)
+        elif variant == "fused_paper":
+            fq.fq_w4a16_outlier_matmul(c.X, Wq, s, z, c.tcs_paper[r], Y=c.Y, ws=ws)
         elif variant == "unfused":
             fq.fq_w4a16_outlier_matmul_unfused(c.X, Wq, s, z, c.tcs[r], Y=c.Y, ws=ws)
         else:
@@ -836,18 +1107,12 @@ def main():
                           "copy_bytes": COPY_CAL_BYTES}), flush=True)
         return
 
+    if args.trace_pass:
+        trace_pass(fq, torch, order, launch, R, dev)
+        return
+
     def capture(fn):
-        g = torch.cuda.CUDAGraph()
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            fn()
-        torch.cuda.current_stream().wait_stream(s)
-        torch.cuda.synchronize()
-        with torch.cuda.graph(g):
-            fn()
-        torch.cuda.synchronize()
-        return g
+        return capture_graph(torch, fn)
 
     # One graph per rotation slot: a whole step on weight copy r.
     graphs = [capture(lambda r=r: [launch(c, r, args.variant) for c in order])
@@ -866,31 +1131,30 @@ def main():
     ms_step = start.elapsed_time(end) / args.steps
     value = step_bytes / (ms_step * 1e-3) / 1e9
 
-    # The same step with the Tile-COO packing this kernel runs fastest on
-    # (by-bucket groups, one bucket per tile: fewest padding slots; the
-    # kernel maps one group per lane and never reads the buckets), reported
-    # beside the headline, whose Tile-COO is the paper kernel's default
-    # (by-column groups, 16 buckets).
-    by_bucket = None
+    # The same step on the paper's Tile-COO format (by-column groups, 16
+    # buckets per tile), reported beside the headline.
+    paper_step = None
     if args.variant == "fused":
-        graphs_b = [capture(lambda r=r: [launch(c, r, "fused_bucket") for c in order])
+        graphs_p = [capture(lambda r=r: [launch(c, r, "fused_paper") for c in order])
                     for r in range(R)]
         for i in range(args.warmup):
-            graphs_b[i % R].replay()
+            graphs_p[i % R].replay()
         torch.cuda.synchronize()
         start.record()
         for i in range(args.steps):
-            graphs_b[i % R].replay()
+            graphs_p[i % R].replay()
         end.record()
         torch.cuda.synchronize()
-        ms_b = start.elapsed_time(end) / args.steps
-        bytes_b = sum(c.bytes_bucket for c in order)
-        by_bucket = {"tilecoo": "by-bucket groups, 1 bucket per tile",
-                     "ms_per_step": round(ms_b, 5), "value": round(bytes_b / (ms_b * 1e-3) / 1e9, 2),
-                     "unit": "GB/s", "step_bytes": bytes_b,
-                     "us_per_matmul": round(ms_b * 1e3 / len(order), 3),
-                     "speedup_vs_by_column": round(ms_step / ms_b, 3)}
-        del graphs_b
+        ms_p = start.elapsed_time(end) / args.steps
+        bytes_p = sum(c.bytes_paper for c in order)
+        paper_step = {"tilecoo": "by-column groups, 16 buckets per tile (the format of the "
+                                 "paper's decoding kernel)",
+                      "ms_per_step": round(ms_p, 5),
+                      "value": round(bytes_p / (ms_p * 1e-3) / 1e9, 2),
+                      "unit": "GB/s", "step_bytes": bytes_p,
+                      "us_per_matmul": round(ms_p * 1e3 / len(order), 3),
+                      "default_speedup": round(ms_p / ms_step, 3)}
+        del graphs_p
 
     # --------------------------------------------- per-matmul durations
     # Each (shape, M) matmul alone: a graph of LPG launches cycling over the
@@ -900,35 +1164,33 @@ def main():
 
     def per_launch_us(c, variant, reps):
         g = capture(lambda: [launch(c, i % R, variant) for i in range(LPG)])
-        warm_replays(torch, g)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / (reps * LPG)
+        return graph_us(torch, g, LPG, reps)
 
     reps = max(2, 160 // LPG)
+    probe = StreamProbe(torch, dev, R)
     details = []
-    fused_total_us = 0.0
     for c in order:
         us = per_launch_us(c, "fused", reps)
-        fused_total_us += us
+        p_us, p_cfg = probe.us(c.bytes)
         d = {"shape": c.name, "M": c.M, "K": c.K, "N": c.N, "bytes": c.bytes,
              "tilecoo_bytes": c.tcs[0].nbytes, "tilecoo_min_bytes": 4 * int(c.tcs[0].sizes.nnz),
+             "tilecoo_paper_format_bytes": c.tcs_paper[0].nbytes,
              "kernel": kernel_name(fq, c.M, c.K, c.N),
              "fused_us": round(us, 3), "fused_GBs": round(c.bytes / us / 1e3, 1),
-             "pct_peak": round(100 * c.bytes / us / 1e3 / HBM_PEAK_GBS, 1)}
+             "pct_peak": round(100 * c.bytes / us / 1e3 / HBM_PEAK_GBS, 1),
+             "probe_us": round(p_us, 3), "probe_GBs": round(c.bytes / p_us / 1e3, 1),
+             "pct_of_probe": round(100 * p_us / us, 1), "probe_config": p_cfg}
         if not args.no_compare:
             d["unfused_us"] = round(per_launch_us(c, "unfused", reps), 3)
             d["dense_only_us"] = round(per_launch_us(c, "dense", reps), 3)
             d["fused_vs_unfused"] = round(d["unfused_us"] / us, 3)
+            d["fused_vs_dense_only"] = round(us / d["dense_only_us"], 3)
         details.append(d)
+    del probe
 
     if not args.no_compare:
-        # hipBLASLt BF16 GEMM comparator on a dense bf16 W of the same shape.
+        # bf16 GEMM comparator: torch.matmul on hipBLASLt with a dense bf16 W
+        # of the same shape (its kernel names: the kernel-trace pass).
         for si, (name, K, N) in enumerate(SHAPES):
             copies = max(2, min(R, int(2.2e9 // (2 * K * N))))
             Ws = [torch.randn(K, N, device=dev, dtype=torch.bfloat16) for _ in range(copies)]
@@ -938,15 +1200,7 @@ def main():
                 x = torch.randn(d["M"], K, device=dev, dtype=torch.bfloat16)
                 out = torch.empty(d["M"], N, device=dev, dtype=torch.bfloat16)
                 g = capture(lambda: [torch.matmul(x, W, out=out) for W in Ws])
-                warm_replays(torch, g)
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record()
-                for _ in range(reps):
-                    g.replay()
-                e1.record()
-                torch.cuda.synchronize()
-                us = e0.elapsed_time(e1) * 1e3 / (reps * copies)
+                us = graph_us(torch, g, copies, reps)
                 d["bf16_gemm_us"] = round(us, 3)
                 # the GEMM's own algorithmic bytes: bf16 W, X and Y
                 d["bf16_gemm_GBs"] = round((2 * K * N + 2 * d["M"] * K + 2 * d["M"] * N) / us / 1e3, 1)
@@ -955,8 +1209,7 @@ def main():
             torch.cuda.empty_cache()
 
     # Dominant kernel: the fused kernel instance that moves most of the
-    # step's bytes (64-column strips with the MFMA outlier mapping: gate+up
-    # and down at M = 4, 8, 16); the other launches are reported beside it.
+    # step's bytes; the other launches are reported beside it.
     dom_name, dom_cases = dominant_kernel(fq, order)
     dom_keys = {(c.name, c.M) for c in dom_cases}
 
@@ -969,6 +1222,14 @@ def main():
     oth_b, oth_t, _ = agg(lambda d: (d["shape"], d["M"]) not in dom_keys)
     traffic_rec = measured_traffic(dom_name)
     achieved = dom_b / (dom_t * 1e-6) / 1e9
+    # layer aggregate: the four linears of one decode layer at each M
+    layers = []
+    for M in MS:
+        b, t, _ = agg(lambda d, M=M: d["M"] == M)
+        pt = sum(d["probe_us"] for d in details if d["M"] == M)
+        layers.append({"M": M, "bytes": b, "fused_us": round(t, 3),
+                       "GBs": round(b / t / 1e3, 1), "pct_peak": round(100 * b / t / 1e3 / HBM_PEAK_GBS, 1),
+                       "pct_of_probe": round(100 * pt / t, 1)})
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -986,7 +1247,8 @@ def main():
             "workload": "Llama-3-8B decode linears qkv 4096x6144, o 4096x4096, "
                         "gate_up 4096x28672, down 14336x4096 at M=1,4,8,16 (16 matmuls "
                         "per step); W_Q INT4 group 128 fp16 scales INT4 zeros; 1% uniform "
-                        "bf16 outliers in Tile-COO 128x64 (16 buckets, by-column); bf16 Y",
+                        "bf16 outliers in Tile-COO 128x64 (library default packing: "
+                        "by-bucket groups, 1 bucket per tile); bf16 Y",
             "variant": args.variant,
             "rotated_weight_copies": R,
             "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
@@ -1005,17 +1267,18 @@ def main():
             "us_per_launch": round(dom_t / max(1, dom_n), 3),
             "other_launches_GBs": round(oth_b / (oth_t * 1e-6) / 1e9, 1) if oth_t else None,
         },
-        "tilecoo_tuned": by_bucket,
+        "layer_aggregate": layers,
+        "tilecoo_paper_format": paper_step,
+        "bf16_gemm_comparator": f"torch.matmul on {blas} (hipBLASLt), bf16 K x N weight",
         "per_matmul": details,
         "pack_s": {k: round(v, 3) for k, v in pack_s.items()},
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(tilecoo_bytes)
+        result["cpu_baseline"] = cpu_baseline(fq)
     if args.details:
         for d in details:
             log(json.dumps(d))
     print(json.dumps(result), flush=True)
-
 
 if __name__ == "__main__":
     main()

@@ -81,10 +81,11 @@ enum { FQ_Y_BF16 = 0, FQ_Y_F32 = 1 };
  *                     n_bank_groups = 4); elems_per_bank * n_bank_groups <= k_tile.
  * The fused kernels need k_tile == 128, n_tile == 64 and k_tile == G.  They map
  * one 16-byte group to one lane and never read the bucket table, so on MI355X
- * the fewest padding slots -- FQ_GROUP_BY_BUCKET with buckets_per_tile = 1 --
- * run fastest (at 1 % outliers: 58 % fewer groups than by-column with 16
- * buckets and about 3 % less time).  The defaults (by-column, 16 buckets) are
- * the format of the paper's kernel.
+ * the fewest padding slots run fastest: the library default is
+ * FQ_GROUP_BY_BUCKET with buckets_per_tile = 1 (only each tile's tail is
+ * padded, Sec. 3.2.1; at 1 % outliers 58 % fewer groups than the by-column
+ * format of the paper's decoding kernel, Sec. 4.2, with 16 buckets).  Every
+ * other grouping and bucket count remains available through these fields.
  */
 typedef struct {
   int32_t k_tile;
@@ -108,8 +109,8 @@ typedef struct {
   int64_t max_tile_groups;  /* largest group count of any single tile */
 } fq_tilecoo_sizes;
 
-/* Library defaults: 128 x 64 tiles, 16 buckets, by-column groups, both
- * reorderings, bank groups (k / 2) % 4. */
+/* Library defaults: 128 x 64 tiles, one bucket per tile, by-bucket groups,
+ * both reorderings, bank groups (k / 2) % 4. */
 fq_tilecoo_params fq_default_tilecoo_params(void);
 
 /*
@@ -168,7 +169,7 @@ fq_status fq_validate_tile_coo(int32_t K, int32_t N, const fq_tilecoo_params* p,
 
 /*
  * fq_quantize_outlier_aware -- offline outlier-aware INT4 quantiser (host; the
- * paper's offline preprocessing, Sec. 2.1 eq. 2-3 and Sec. 3).
+ * paper's offline preprocessing, Sec. 2.2 eq. 2-3 and Sec. 3).
  *   W            fp32 [K][N] row-major, finite (FQ_ERR_RANGE otherwise).
  *   group_size   quantisation group along K; K % group_size == 0, K % 8 == 0,
  *                N % 8 == 0 (FQ_ERR_SHAPE otherwise).
@@ -220,7 +221,7 @@ typedef struct {
 
 /*
  * Problem description for the device entry points.
- *   M           rows of X and Y, >= 1; the kernels implement 1..32
+ *   M           rows of X and Y, >= 1; the kernels implement 1..128
  *               (FQ_ERR_UNSUPPORTED above).
  *   K, N        K % 128 == 0, N % 64 == 0.  The kernels address every array
  *               with 32-bit byte offsets: Wq (K N / 2 bytes), X (2 M K bytes),

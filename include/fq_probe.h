@@ -1,0 +1,50 @@
+/*
+ * fq_probe.h -- C ABI of the streaming-read probe that measures the HBM read
+ * bandwidth attainable on one MI355X at a given byte count.  It is a
+ * measurement reference for the matmul kernels of fq.h (their algorithmic
+ * bytes divided by their time, set against what a plain read of the same
+ * number of bytes achieves), not part of the operator: FlashQuant
+ * (arXiv 2608.15531) argues that decode-time matmuls are bound by memory
+ * bandwidth (Sec. 2.1 on decoding, and the arithmetic-intensity argument at
+ * the opening of Sec. 3), and this probe gives that bound its measured value
+ * at each size.
+ *
+ * Built into its own library, libfqprobe.so.
+ */
+#ifndef FQ_PROBE_H
+#define FQ_PROBE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * fq_probe_stream_read -- enqueue one kernel that reads `bytes` bytes starting
+ * at `src` once, with 16-byte vector loads, and writes nothing but a
+ * checksum word per workgroup that is almost never stored (so the loads
+ * cannot be optimised away).
+ *   src              device pointer, 16-byte aligned; bytes % 16 == 0, bytes > 0,
+ *                    bytes < 2^40.
+ *   workgroups       grid size, 1..65536; workgroup w reads the contiguous
+ *                    share [w, w+1) * ceil(bytes / 16 / workgroups) of the
+ *                    16-byte words.
+ *   waves            wave64s per workgroup: 1, 2, 4, 8 or 16.
+ *   loads_in_flight  independent 16-byte loads per lane issued before any is
+ *                    consumed: 1, 2, 4 or 8.
+ *   sink             device pointer to `workgroups` uint32 words (4-byte
+ *                    aligned); contents unspecified after the call.
+ *   stream           hipStream_t (NULL: the default stream).
+ * Returns 0 on success, 1 on a bad argument (nothing launched), 2 when the
+ * HIP runtime reported a launch error.
+ */
+int fq_probe_stream_read(const void* src, size_t bytes, int32_t workgroups, int32_t waves,
+                         int32_t loads_in_flight, uint32_t* sink, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FQ_PROBE_H */

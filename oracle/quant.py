@@ -5,10 +5,10 @@ imports it and it imports nothing from the library.
 
 Paper references (FlashQuant, arXiv 2608.15531):
 
-* eq. (2) (Sec. 2.1, Outlier-Aware Quantization): q = round(w / s) + z with
+* eq. (2) (Sec. 2.2, Outlier-Aware Quantization): q = round(w / s) + z with
   s = (w_max - w_min) / (2^b - 1) and z = round(-w_min / s); eq. (3):
   w_hat = s (q - z).
-* Sec. 2.1: outliers are the high-magnitude weights, kept in bf16.
+* Sec. 2.2: outliers are the high-magnitude weights, kept in bf16.
 * Sec. 3.2.1: padding slots of the packed groups may hold original weights.
 
 Readings where the paper is silent (kept in the design notes as well):

@@ -312,7 +312,9 @@ def _stream_handle(stream, device) -> int:
 
 
 def workspace(nbytes: int, device, stream_handle: int):
-    """Zero-filled workspace kept per (device, stream); the kernels leave it zeroed."""
+    """Zero-filled workspace kept per (device, stream); the kernels leave it zeroed.
+    Call it with the kernel's stream current (see _on_stream): the allocation
+    and its zero fill are then ordered before the kernel on that stream."""
     torch = _torch()
     key = (torch.device(device).index, stream_handle)
     buf = _workspaces.get(key)
@@ -320,6 +322,16 @@ def workspace(nbytes: int, device, stream_handle: int):
         buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
         _workspaces[key] = buf
     return buf
+
+
+def _on_stream(stream):
+    """Makes `stream` current while Y and the workspace are allocated, so the
+    caching allocator ties them to the stream the kernel runs on and the
+    workspace's zero fill precedes the kernel there."""
+    import contextlib
+    if stream is None:
+        return contextlib.nullcontext()
+    return _torch().cuda.stream(stream)
 
 
 def _problem(M, K, N, y_dtype, split_k, group=128, sparse="auto", flags=0) -> fq_problem:
@@ -358,13 +370,14 @@ def fq_w4a16_outlier_matmul(X, Wq, scales, zeros, tc: TileCOODevice, Y=None, y_d
     """Fused Y = X dequant(W_Q) + X W_O on the GPU; returns Y.  flags: any of
     FQ_SCHED_STREAM_K, FQ_FOUR_WAVES."""
     lib = load()
-    M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
-    pr = _problem(M, K, N, ydt, split_k, group, sparse, flags)
-    need = C.c_size_t(0)
-    _check(lib.fq_workspace_bytes(C.byref(pr), C.byref(need)), "fq_workspace_bytes")
-    sh = _stream_handle(stream, X.device)
-    if ws is None:
-        ws = workspace(need.value, X.device, sh)
+    with _on_stream(stream):
+        M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
+        pr = _problem(M, K, N, ydt, split_k, group, sparse, flags)
+        need = C.c_size_t(0)
+        _check(lib.fq_workspace_bytes(C.byref(pr), C.byref(need)), "fq_workspace_bytes")
+        sh = _stream_handle(stream, X.device)
+        if ws is None:
+            ws = workspace(need.value, X.device, sh)
     tcs = tc.struct()
     _check(lib.fq_w4a16_outlier_matmul(C.byref(pr), X.data_ptr(), Wq.data_ptr(),
                                        scales.data_ptr(), zeros.data_ptr(), C.byref(tcs),
@@ -378,14 +391,15 @@ def fq_w4a16_outlier_matmul_unfused(X, Wq, scales, zeros, tc: TileCOODevice, Y=N
                                     group: int = 128, sparse: str = "auto", flags: int = 0):
     """Two-kernel baseline (dense W4A16 then Tile-COO SpMM); returns Y."""
     lib = load()
-    M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
-    pr = _problem(M, K, N, ydt, split_k, group, sparse, flags)
-    need = C.c_size_t(0)
-    _check(lib.fq_workspace_bytes_unfused(C.byref(pr), C.byref(need)),
-           "fq_workspace_bytes_unfused")
-    sh = _stream_handle(stream, X.device)
-    if ws is None:
-        ws = workspace(need.value, X.device, sh)
+    with _on_stream(stream):
+        M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
+        pr = _problem(M, K, N, ydt, split_k, group, sparse, flags)
+        need = C.c_size_t(0)
+        _check(lib.fq_workspace_bytes_unfused(C.byref(pr), C.byref(need)),
+               "fq_workspace_bytes_unfused")
+        sh = _stream_handle(stream, X.device)
+        if ws is None:
+            ws = workspace(need.value, X.device, sh)
     tcs = tc.struct()
     _check(lib.fq_w4a16_outlier_matmul_unfused(C.byref(pr), X.data_ptr(), Wq.data_ptr(),
                                                scales.data_ptr(), zeros.data_ptr(),
@@ -399,13 +413,14 @@ def fq_w4a16_matmul(X, Wq, scales, zeros, Y=None, y_dtype="bf16", split_k: int =
                     stream=None, ws=None, group: int = 128, flags: int = 0):
     """Dense-only Y = X dequant(W_Q) (outliers ignored); returns Y."""
     lib = load()
-    M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
-    pr = _problem(M, K, N, ydt, split_k, group, flags=flags)
-    need = C.c_size_t(0)
-    _check(lib.fq_workspace_bytes(C.byref(pr), C.byref(need)), "fq_workspace_bytes")
-    sh = _stream_handle(stream, X.device)
-    if ws is None:
-        ws = workspace(need.value, X.device, sh)
+    with _on_stream(stream):
+        M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
+        pr = _problem(M, K, N, ydt, split_k, group, flags=flags)
+        need = C.c_size_t(0)
+        _check(lib.fq_workspace_bytes(C.byref(pr), C.byref(need)), "fq_workspace_bytes")
+        sh = _stream_handle(stream, X.device)
+        if ws is None:
+            ws = workspace(need.value, X.device, sh)
     _check(lib.fq_w4a16_matmul(C.byref(pr), X.data_ptr(), Wq.data_ptr(), scales.data_ptr(),
                                zeros.data_ptr(), Y.data_ptr(), ws.data_ptr(), ws.numel(), sh),
            "fq_w4a16_matmul")
@@ -418,9 +433,10 @@ def fq_debug_decode_tile_coo(tc: TileCOODevice, K: int, N: int, stream=None):
     lib = load()
     dev = tc.packed.device
     G = tc.n_groups
-    k = torch.empty(max(4 * G, 1), dtype=torch.int32, device=dev)
-    n = torch.empty(max(4 * G, 1), dtype=torch.int32, device=dev)
-    v = torch.empty(max(4 * G, 1), dtype=torch.int16, device=dev)
+    with _on_stream(stream):
+        k = torch.empty(max(4 * G, 1), dtype=torch.int32, device=dev)
+        n = torch.empty(max(4 * G, 1), dtype=torch.int32, device=dev)
+        v = torch.empty(max(4 * G, 1), dtype=torch.int16, device=dev)
     tcs = tc.struct()
     _check(lib.fq_debug_decode_tile_coo(C.byref(tcs), K, N, k.data_ptr(), n.data_ptr(),
                                         v.data_ptr(), _stream_handle(stream, dev)),
@@ -429,9 +445,16 @@ def fq_debug_decode_tile_coo(tc: TileCOODevice, K: int, N: int, stream=None):
 
 
 def fq_launch_config(M: int, K: int, N: int, split_k: int = 0, sparse: str = "auto",
-                     flags: int = 0, buckets_per_tile: int = 16, group_mode: int = 0) -> dict:
-    """The launch the fused entry point would make (nothing is launched)."""
+                     flags: int = 0, buckets_per_tile: int | None = None,
+                     group_mode: int | None = None) -> dict:
+    """The launch the fused entry point would make (nothing is launched) for a
+    Tile-COO packed with the given bucket count and grouping (default: the
+    library's default packing)."""
     lib = load()
+    if buckets_per_tile is None or group_mode is None:
+        d = lib.fq_default_tilecoo_params()
+        buckets_per_tile = d.buckets_per_tile if buckets_per_tile is None else buckets_per_tile
+        group_mode = d.group_mode if group_mode is None else group_mode
     pr = _problem(M, K, N, FQ_Y_BF16, split_k, 128, sparse, flags)
     cfg = (C.c_int32 * 9)()
     _check(lib.fq_launch_config(C.byref(pr), buckets_per_tile, group_mode, cfg),

@@ -14,6 +14,10 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_NAME = "libfq.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
+# the streaming-read probe (a measurement reference, include/fq_probe.h) is a
+# library of its own
+PROBE_LIB_PATH = os.path.join(HERE, "libfqprobe.so")
+PROBE_SOURCES = ["probe.hip"]
 
 HOST_SOURCES = ["capi.cpp", "tilecoo.cpp", "quant.cpp"]
 HIP_SOURCES = ["kernels.hip"]
@@ -43,22 +47,26 @@ def _run(cmd, verbose):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link libfq.so next to this file; returns its path."""
+    """Compile every source and link libfq.so and libfqprobe.so next to this
+    file; returns the path of libfq.so."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     incs = ["-I", INCLUDE, "-I", CSRC]
     jobs = []
     for src in HOST_SOURCES:
         obj = os.path.join(BUILD_DIR, src + ".o")
         jobs.append(["g++", *HOST_FLAGS, *incs, "-c", os.path.join(CSRC, src), "-o", obj])
-    for src in HIP_SOURCES:
+    for src in HIP_SOURCES + PROBE_SOURCES:
         obj = os.path.join(BUILD_DIR, src + ".o")
         jobs.append([_hipcc(), *HIP_FLAGS, *incs, "-c", os.path.join(CSRC, src), "-o", obj])
     with ThreadPoolExecutor(max_workers=4) as ex:
         list(ex.map(lambda c: _run(c, verbose), jobs))
     objs = [j[-1] for j in jobs]
-    tmp = LIB_PATH + ".tmp"
-    _run([_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
-    shutil.move(tmp, LIB_PATH)
+    probe_objs = [o for o in objs if os.path.basename(o)[:-2] in PROBE_SOURCES]
+    lib_objs = [o for o in objs if o not in probe_objs]
+    for path, ob in ((LIB_PATH, lib_objs), (PROBE_LIB_PATH, probe_objs)):
+        tmp = path + ".tmp"
+        _run([_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *ob, "-o", tmp], verbose)
+        shutil.move(tmp, path)
     return LIB_PATH
 
 

@@ -1195,6 +1195,15 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   // twelve waves of 64-column tiles with two 16-row blocks exceed the
   // registers of three waves per SIMD
   if (p.NCB == 4 && p.MB == 2 && p.NW == 8) p.NWS = 0;
+  if (p.NWS > 0) {
+    // the outlier waves split the same K range among half as many waves, and
+    // each indexes its tiles' group offsets from one register: at most 63
+    // tiles per outlier wave, so the split grows where K is long
+    const int S = std::max(p.S, (p.T + p.NWS * 63 - 1) / (p.NWS * 63));
+    p.S = std::min(S, p.T);
+    p.G = p.n_strips * p.S;
+    p.C = p.S;
+  }
 
   if (p.MODE == 0) {
     p.slot_bytes = align_up(size_t(p.slab_M) * kXStride * 2, 16);

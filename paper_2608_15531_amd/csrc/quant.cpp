@@ -1,6 +1,6 @@
 // Offline outlier-aware INT4 quantiser (host).  Splits a dense weight matrix
 // into the low-bit part W_Q (per-group affine INT4, eq. 2 and eq. 3 of the
-// paper) and the bf16 outlier part W_O (the highest-magnitude weights, Sec. 2.1),
+// paper) and the bf16 outlier part W_O (the highest-magnitude weights, Sec. 2.2),
 // and optionally stores original weights in the Tile-COO padding slots
 // (Sec. 3.2.1: padding slots may hold original weight values).
 #include <algorithm>

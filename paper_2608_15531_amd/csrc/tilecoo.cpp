@@ -247,8 +247,8 @@ fq_tilecoo_params fq_default_tilecoo_params(void) {
   fq_tilecoo_params p;
   p.k_tile = 128;
   p.n_tile = 64;
-  p.buckets_per_tile = 16;
-  p.group_mode = FQ_GROUP_BY_COLUMN;
+  p.buckets_per_tile = 1;
+  p.group_mode = FQ_GROUP_BY_BUCKET;
   p.reorder = FQ_REORDER_COLUMNS | FQ_REORDER_ELEMENTS;
   p.elems_per_bank = 2;
   p.n_bank_groups = 4;

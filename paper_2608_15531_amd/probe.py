@@ -1,0 +1,47 @@
+"""Binding of libfqprobe.so, the streaming-read probe declared in
+include/fq_probe.h (a measurement reference for the matmul kernels; argument
+marshalling only).  Raises if the library has not been built."""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+import threading
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+PROBE_LIB_PATH = os.path.join(_HERE, "libfqprobe.so")
+EXPORTS = ("fq_probe_stream_read",)
+
+_lib = None
+_lock = threading.Lock()
+
+
+def load() -> C.CDLL:
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(PROBE_LIB_PATH):
+                raise ImportError(f"libfqprobe.so is not built ({PROBE_LIB_PATH}); run "
+                                  "paper_2608_15531_amd.build.build() first")
+            lib = C.CDLL(PROBE_LIB_PATH)
+            lib.fq_probe_stream_read.argtypes = [C.c_void_p, C.c_size_t, C.c_int32, C.c_int32,
+                                                 C.c_int32, C.c_void_p, C.c_void_p]
+            lib.fq_probe_stream_read.restype = C.c_int
+            _lib = lib
+    return _lib
+
+
+def fq_probe_stream_read(src, nbytes: int, workgroups: int, waves: int, loads_in_flight: int,
+                         sink, stream=None) -> None:
+    """Enqueue one streaming read of nbytes of the device tensor src on
+    `stream` (torch stream, default: current).  sink: device tensor of at
+    least `workgroups` int32 words."""
+    import torch
+    if nbytes > src.numel() * src.element_size() or sink.numel() * sink.element_size() < 4 * workgroups:
+        raise ValueError("fq_probe_stream_read: buffer too small")
+    if stream is None:
+        stream = torch.cuda.current_stream(src.device)
+    rc = load().fq_probe_stream_read(src.data_ptr(), nbytes, workgroups, waves,
+                                     loads_in_flight, sink.data_ptr(), int(stream.cuda_stream))
+    if rc != 0:
+        raise RuntimeError(f"fq_probe_stream_read failed ({rc})")

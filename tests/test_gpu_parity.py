@@ -127,8 +127,10 @@ EXACT_CASES = [
     (9, 1152, 448, 0.03, 0, c_params()),
     # one row with by-bucket groups: the default mapping is MFMA here
     (1, 2048, 1024, 0.02, 0, c_params(group_mode=1)),
-    # the packing this kernel runs fastest on: by-bucket groups, one bucket per tile
+    # the library default packing: by-bucket groups, one bucket per tile
     (8, 1024, 512, 0.02, 0, c_params(group_mode=1, buckets_per_tile=1)),
+    (1, 4096, 4096, 0.01, 0, c_params(group_mode=1, buckets_per_tile=1)),
+    (16, 4096, 4096, 0.01, 0, c_params(group_mode=1, buckets_per_tile=1)),
     # more than 32 rows: 32-row slabs in the grid, ragged last slab, split-K
     (33, 1024, 256, 0.02, 0, c_params()),
     (64, 2048, 512, 0.01, 3, c_params()),
@@ -306,6 +308,46 @@ def test_repeat_calls_bit_identical(gpu_lib):
     assert np.array_equal(a, b)
 
 
+def test_repeat_calls_bit_identical_gather_mapping(gpu_lib):
+    """The gather mapping adds products with LDS float atomics into per-wave
+    buffers; a wave's LDS operations complete in issue order, so repeated
+    calls give identical bits.  gate+up at one row, by-column groups (the
+    gather mapping's own packing), as the benchmark would launch it."""
+    fq = gpu_lib
+    K, N = 4096, 28672
+    prob = make_problem(1, K, N, frac=0.01, seed=seed_for(1, 2, 0))
+    assert fq.fq_launch_config(1, K, N, group_mode=0, buckets_per_tile=16)["mapping"] == "gather"
+    X, Wq, s, z = fq.to_device(prob)
+    tc = fq.TileCOODevice(fq.fq_pack_tile_coo(K, N, prob.k, prob.n, prob.v, c_params()))
+    outs = []
+    for _ in range(3):
+        y = fq.fq_w4a16_outlier_matmul(X, Wq, s, z, tc, y_dtype="f32", sparse="gather")
+        torch.cuda.synchronize()
+        outs.append(y.cpu().numpy())
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+
+
+@pytest.mark.parametrize("flags", [64 | 8, 64 | 32, 64], ids=["sparse_waves+four_waves",
+                                                             "sparse_waves+strip64",
+                                                             "sparse_waves"])
+@pytest.mark.parametrize("M", [4, 32])
+def test_exact_outlier_waves_long_k(gpu_lib, flags, M):
+    """Outlier waves beside the dense waves with K = 28672 (224 tiles per strip)
+    and no split requested: the outlier waves share each K range among half
+    as many waves, so the planner must keep them at 63 tiles or fewer each
+    (one register of group offsets per wave).  Exact arithmetic, bit for bit."""
+    fq = gpu_lib
+    K, N = 28672, 128
+    cfg = fq.fq_launch_config(M, K, N, split_k=1, flags=flags)
+    T = K // 128
+    if cfg["outlier_waves"]:
+        assert -(-(-(-T // cfg["split_k"])) // cfg["outlier_waves"]) <= 63, cfg
+    log(f"exact outlier waves K={K} N={N} M={M} flags={flags} cfg={cfg}")
+    prob = make_exact_problem(M, K, N, frac=0.01, seed=M + flags)
+    y = run(fq, prob, "fused", "f32", c_params(), split_k=1, sparse="mfma", flags=flags)
+    assert np.array_equal(y, ref(prob).astype(np.float32))
+
+
 def test_workspace_counters_rearmed(gpu_lib):
     fq = gpu_lib
     prob = make_problem(4, 4096, 4096, frac=0.01, seed=8)
@@ -345,27 +387,41 @@ def test_workspace_shared_across_shapes(gpu_lib):
 FULL_SHAPES = [(4096, 6144), (4096, 4096), (4096, 28672), (14336, 4096)]
 
 
+# (M, strip flag, packing): every row count of the benchmark in the default
+# launch configuration with the default packing (what bench.py times), the
+# paper's by-column packing (the gather mapping at one row), and each strip
+# width forced
+PAPER_FORMAT = {"buckets_per_tile": 16, "group_mode": 0}
+FULL_CASES = ([(M, 0, None) for M in (1, 4, 8, 16)]
+              + [(M, 0, "paper") for M in (1, 4)]
+              + [(M, f, None) for M in (1, 16) for f in (16, 32)])
+
+
 @pytest.mark.parametrize("shape", FULL_SHAPES, ids=["qkv", "o", "gate_up", "down"])
-@pytest.mark.parametrize("M", [1, 16])
-@pytest.mark.parametrize("strip", [0, 16, 32], ids=["auto", "strip32", "strip64"])
-def test_full_size_sampled_columns(gpu_lib, shape, M, strip):
+@pytest.mark.parametrize("case", FULL_CASES,
+                         ids=[f"M{M}-{ {0: 'auto', 16: 'strip32', 32: 'strip64'}[f]}-"
+                              f"{pk or 'default'}" for M, f, pk in FULL_CASES])
+def test_full_size_sampled_columns(gpu_lib, shape, case):
     """Llama-3-8B decode linears at full size, in the launch configuration the
-    benchmark times (auto) and with each strip width forced; the oracle
+    benchmark times (auto, default packing) at every row count, with the
+    paper's by-column packing, and with each strip width forced; the oracle
     computes a sample of columns one by one."""
+    M, strip, packing = case
     K, N = shape
-    log(f"full K={K} N={N} M={M} strip flag={strip}")
+    params = PAPER_FORMAT if packing == "paper" else None
+    log(f"full K={K} N={N} M={M} strip flag={strip} packing={packing or 'default'}")
     prob = make_problem(M, K, N, frac=0.01, seed=seed_for(1, FULL_SHAPES.index(shape),
                                                            [1, 4, 8, 16].index(M)))
     rng = np.random.default_rng(K + N + M)
     cols = np.unique(np.concatenate([[0, 63, 64, N - 1], rng.choice(N, 192, replace=False)]))
     y_ref = ref(prob, cols)
     sparse = "mfma" if strip == 16 else "auto"
-    y16 = run(gpu_lib, prob, "fused", "bf16", sparse=sparse, flags=strip)
+    y16 = run(gpu_lib, prob, "fused", "bf16", params=params, sparse=sparse, flags=strip)
     assert_bf16_close(y16[:, cols], y_ref)
-    y32 = run(gpu_lib, prob, "fused", "f32", sparse=sparse, flags=strip)
+    y32 = run(gpu_lib, prob, "fused", "f32", params=params, sparse=sparse, flags=strip)
     assert_f32_close(y32[:, cols], y_ref)
     # property that holds at any size: fused and unfused agree closely everywhere
-    yu = run(gpu_lib, prob, "unfused", "f32", sparse=sparse, flags=strip)
+    yu = run(gpu_lib, prob, "unfused", "f32", params=params, sparse=sparse, flags=strip)
     rel = np.linalg.norm(yu - y32) / np.linalg.norm(y32)
     assert rel <= F32_FROB
 
@@ -427,10 +483,11 @@ def _problem_70b(shape, M):
 
 
 @pytest.mark.parametrize("shape", SHAPES_70B, ids=["qkv70", "o70", "gate_up70", "down70"])
-@pytest.mark.parametrize("M", [1, 32])
+@pytest.mark.parametrize("M", [1, 8, 16, 32])
 def test_70b_full_size_sampled_columns(gpu_lib, shape, M):
-    """Llama-3-70B decode linears at full size (M = 1: gather mapping; M = 32:
-    two 16-row MFMA blocks); sampled columns against the oracle."""
+    """Llama-3-70B decode linears at full size, every row count of that sweep,
+    in the default launch configuration and packing (M = 32: two 16-row MFMA
+    blocks); sampled columns against the oracle."""
     K, N = shape
     log(f"70B K={K} N={N} M={M}")
     prob = _problem_70b(shape, M)

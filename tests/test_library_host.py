@@ -40,9 +40,31 @@ def test_exports_every_declared_symbol(lib):
         assert getattr(lib, name) is not None
 
 
+def test_probe_library_exports_its_header(lib):
+    """libfqprobe.so (the streaming-read probe) exports what include/fq_probe.h
+    declares, and rejects bad arguments on the host without launching."""
+    from paper_2608_15531_amd import probe
+    with open(os.path.join(ROOT, "include", "fq_probe.h")) as f:
+        header = f.read()
+    declared = set(re.findall(r"^\s*int\s+(fq_\w+)\(", header, re.M))
+    assert declared == set(probe.EXPORTS)
+    plib = probe.load()
+    for name in declared:
+        assert getattr(plib, name) is not None
+    buf = (C.c_uint32 * 128)()
+    addr = (C.addressof(buf) + 15) & ~15   # 16-byte aligned: only the named argument is bad
+    f = plib.fq_probe_stream_read
+    assert f(None, 256, 1, 1, 1, addr, None) == 1                # null source
+    assert f(addr, 0, 1, 1, 1, addr, None) == 1                  # no bytes
+    assert f(addr, 100, 1, 1, 1, addr, None) == 1                # not a multiple of 16
+    assert f(addr, 256, 0, 1, 1, addr, None) == 1                # no workgroups
+    assert f(addr, 256, 1, 3, 1, addr, None) == 1                # bad wave count
+    assert f(addr, 256, 1, 1, 3, addr, None) == 1                # bad loads in flight
+
+
 def test_default_params(lib):
     p = fq.fq_default_tilecoo_params().as_dict()
-    assert p == {"k_tile": 128, "n_tile": 64, "buckets_per_tile": 16, "group_mode": 0,
+    assert p == {"k_tile": 128, "n_tile": 64, "buckets_per_tile": 1, "group_mode": 1,
                  "reorder": 3, "elems_per_bank": 2, "n_bank_groups": 4}
 
 
@@ -195,14 +217,18 @@ def _corrupt_cases(tc):
     yield "duplicate", ti, bi, p5.ravel()
 
 
+# the format of the paper's decoding kernel: by-column groups, 16 buckets per tile
+PAPER_FORMAT = {"buckets_per_tile": 16, "group_mode": 0}
+
+
 def test_validate_rejects_corruption(lib):
     prob = make_problem(1, 512, 256, frac=0.03, seed=17)
-    tc = fq.fq_pack_tile_coo(512, 256, prob.k, prob.n, prob.v)
-    fq.fq_validate_tile_coo(512, 256, None, tc.tile_indptr, tc.bucket_info, tc.packed)
+    tc = fq.fq_pack_tile_coo(512, 256, prob.k, prob.n, prob.v, PAPER_FORMAT)
+    fq.fq_validate_tile_coo(512, 256, tc.params, tc.tile_indptr, tc.bucket_info, tc.packed)
     names = []
     for name, ti, bi, pk in _corrupt_cases(tc):
         with pytest.raises(fq.FqError) as e:
-            fq.fq_validate_tile_coo(512, 256, None, ti, bi, pk)
+            fq.fq_validate_tile_coo(512, 256, tc.params, ti, bi, pk)
         assert e.value.name == "FQ_ERR_FORMAT", name
         names.append(name)
     assert len(names) >= 7
@@ -224,12 +250,16 @@ def test_validate_rejects_shared_column(lib):
 
 def test_storage_formula_on_library_output(lib):
     prob = make_problem(1, 4096, 4096, frac=0.01, seed=0)
-    tc = fq.fq_pack_tile_coo(4096, 4096, prob.k, prob.n, prob.v)
-    s = tc.sizes
-    assert s.n_tiles == 2048 and s.n_buckets == 2048 * 16 and s.nnz == 167772
-    assert s.bytes == oracle.storage_bytes(s.n_tiles, s.n_buckets, 4 * s.n_groups)
-    # padded Tile-COO still beats the paper's CSR count at 1 %
-    assert s.bytes < oracle.csr_bytes(4096, s.nnz)
+    for params, buckets in ((PAPER_FORMAT, 16), (None, 1)):
+        tc = fq.fq_pack_tile_coo(4096, 4096, prob.k, prob.n, prob.v, params)
+        s = tc.sizes
+        assert s.n_tiles == 2048 and s.n_buckets == 2048 * buckets and s.nnz == 167772
+        assert s.bytes == oracle.storage_bytes(s.n_tiles, s.n_buckets, 4 * s.n_groups)
+        # padded Tile-COO still beats the paper's CSR count at 1 %
+        assert s.bytes < oracle.csr_bytes(4096, s.nnz)
+    # the default (by-bucket, one bucket per tile) pads only each tile's tail:
+    # fewer than 4 padding slots per tile
+    assert s.n_pad < 4 * s.n_tiles
 
 
 # ---------------------------------------------------- device entry points --
@@ -329,8 +359,10 @@ def test_debug_decode_rejects(lib):
 # ----------------------------------------------------- launch configuration --
 
 @pytest.mark.parametrize("M,K,N,expect", [
-    # wide matrices: 64-column strips, no split; the gather mapping at M = 1
-    (1, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="gather")),
+    # wide matrices: 64-column strips, no split; the gather mapping at M = 1 with
+    # by-column groups, the MFMA mapping with the default by-bucket groups
+    (1, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="gather", group_mode=0)),
+    (1, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="mfma")),
     (16, 4096, 28672, dict(strip_cols=64, split_k=1, mapping="mfma", x_stage_loads=4)),
     # narrow, K <= 8192: 32-column strips without split-K
     (1, 4096, 4096, dict(strip_cols=32, split_k=1, dense_waves=8, mapping="mfma", x_stage_loads=1)),
@@ -352,9 +384,11 @@ def test_debug_decode_rejects(lib):
     (128, 4096, 14336, dict(x_stage_loads=8)),
     # 160+ 64-column strips: 64-column strips, no split, eight waves
     (8, 4096, 14336, dict(strip_cols=64, split_k=1, dense_waves=8)),
-    (1, 8192, 10240, dict(strip_cols=64, mapping="gather", x_staged=False)),
-    # the gather mapping stages its own X slice
-    (1, 4096, 28672, dict(mapping="gather", x_stage_loads=0)),
+    (1, 8192, 10240, dict(strip_cols=64, mapping="gather", x_staged=False, group_mode=0)),
+    # the gather mapping (by-column groups at one row) stages its own X slice
+    (1, 4096, 28672, dict(mapping="gather", x_stage_loads=0, group_mode=0)),
+    # the default packing (by-bucket groups) takes the MFMA mapping at one row too
+    (1, 4096, 28672, dict(mapping="mfma", x_stage_loads=1)),
     # long K: 64-column strips split to about 512 workgroups
     (4, 14336, 4096, dict(strip_cols=64, split_k=8, dense_waves=4, workgroups=512)),
     # two 16-row blocks where four-wave workgroups would overflow one round:
@@ -367,7 +401,9 @@ def test_debug_decode_rejects(lib):
     (32, 28672, 8192, dict(strip_cols=64, split_k=2, dense_waves=8, workgroups=256)),
 ])
 def test_launch_config_defaults(lib, M, K, N, expect):
-    cfg = fq.fq_launch_config(M, K, N)
+    expect = dict(expect)
+    gm = expect.pop("group_mode", None)
+    cfg = fq.fq_launch_config(M, K, N, group_mode=gm, buckets_per_tile=None if gm is None else 16)
     for k, v in expect.items():
         assert cfg[k] == v, (k, cfg)
     assert cfg["outlier_waves"] == 0 and not cfg["stream_k"]
@@ -382,8 +418,9 @@ def test_launch_config_switches(lib):
     assert fq.fq_launch_config(4, 4096, 28672, flags=fq.FQ_SCHED_STREAM_K)["stream_k"]
     assert fq.fq_launch_config(4, 4096, 4096, split_k=3)["split_k"] == 3
     # groups spanning columns (by-bucket) take the MFMA mapping at M = 1 too
-    assert fq.fq_launch_config(1, 4096, 28672)["mapping"] == "gather"
+    assert fq.fq_launch_config(1, 4096, 28672, group_mode=fq.FQ_GROUP_BY_COLUMN)["mapping"] == "gather"
     assert fq.fq_launch_config(1, 4096, 28672, group_mode=fq.FQ_GROUP_BY_BUCKET)["mapping"] == "mfma"
+    assert fq.fq_launch_config(1, 4096, 28672)["mapping"] == "mfma"   # default: by-bucket
     assert fq.fq_launch_config(1, 4096, 28672, sparse="gather",
                                group_mode=fq.FQ_GROUP_BY_BUCKET)["mapping"] == "gather"
     with pytest.raises(fq.FqError):
@@ -405,7 +442,10 @@ def test_launch_plans_stay_within_kernel_limits(lib):
     Ks = [128, 256, 1024, 4096, 8192, 14336, 28672, 57344]
     Ns = [64, 128, 192, 512, 4096, 6144, 14336, 28672, 57344]
     switches = [0, fq.FQ_STRIP_32, fq.FQ_STRIP_64, fq.FQ_FOUR_WAVES, fq.FQ_SCHED_STREAM_K,
-                fq.FQ_SPARSE_WAVES, fq.FQ_STRIP_32 | fq.FQ_FOUR_WAVES]
+                fq.FQ_SPARSE_WAVES, fq.FQ_STRIP_32 | fq.FQ_FOUR_WAVES,
+                fq.FQ_SPARSE_WAVES | fq.FQ_FOUR_WAVES, fq.FQ_SPARSE_WAVES | fq.FQ_STRIP_64,
+                fq.FQ_SPARSE_WAVES | fq.FQ_STRIP_32,
+                fq.FQ_SCHED_STREAM_K | fq.FQ_FOUR_WAVES]
     accepted = 0
     for M in Ms:
         for K in Ks:
@@ -439,4 +479,14 @@ def test_launch_plans_stay_within_kernel_limits(lib):
                             slabs = -(-M // 32)
                             assert c["workgroups"] == N // c["strip_cols"] * S * slabs, where
                             assert -(-(-(-T // S)) // c["dense_waves"]) <= 63, where
+                            if c["outlier_waves"]:
+                                # the outlier waves share the same K range among half as
+                                # many waves: the same one-register bound applies to them
+                                assert -(-(-(-T // S)) // c["outlier_waves"]) <= 63, where
+                        else:
+                            # Stream-K: a workgroup's segment lies in one strip and holds
+                            # at most its even share of the units
+                            U = N // c["strip_cols"] * T
+                            share = min(T, -(-U // c["workgroups"]))
+                            assert -(-share // c["dense_waves"]) <= 63, where
     assert accepted > 10000

@@ -435,3 +435,67 @@ def test_element_reordering_reduces_bank_group_collisions():
     ca = sum(oracle.oracle.bank_group_collisions(a, t) for t in range(a.n_tiles))
     cb = sum(oracle.oracle.bank_group_collisions(b, t) for t in range(b.n_tiles))
     assert cb < ca
+
+
+def test_bank_group_collisions_hand_counted():
+    """The collision metric of Sec. 3.2.2 on a hand-written tile whose counts
+    were worked out by hand (tests/golden/bank_collisions_hand.json), for two
+    bank geometries and three lockstep widths."""
+    with open(os.path.join(GOLDEN, "bank_collisions_hand.json")) as f:
+        g = json.load(f)
+    words = []
+    for rows, cols in g["groups"]:
+        words += [sum(r << (8 * j) for j, r in enumerate(rows)),
+                  sum(c << (8 * j) for j, c in enumerate(cols)), 0x3F803F80, 0x3F803F80]
+    for e in g["expected"]:
+        params = oracle.Params(k_tile=128, n_tile=64, buckets=g["buckets"],
+                               group_mode=oracle.BY_BUCKET, reorder=0,
+                               elems_per_bank=e["elems_per_bank"],
+                               n_bank_groups=e["n_bank_groups"])
+        tc = oracle.TileCOO(params, np.array(g["tile_indptr"], np.uint32),
+                            np.array(g["bucket_info"], np.uint16),
+                            np.array(words, np.uint32), nnz=4 * len(g["groups"]))
+        got = oracle.oracle.bank_group_collisions(tc, 0, e["lanes_per_step"])
+        assert got == e["collisions"], e
+
+
+@pytest.mark.parametrize("params", [oracle.Params(),
+                                    oracle.Params(buckets=1, group_mode=oracle.BY_BUCKET),
+                                    oracle.Params(buckets=8, group_mode=oracle.BY_BUCKET,
+                                                  reorder=0)])
+def test_matmul_through_tile_coo_equals_bruteforce(params):
+    """eq. (1) with W_O read back through the oracle's own Tile-COO (pack then
+    unpack) against scalar sums over the dense reconstruction W_hat + W_O,
+    and bit for bit against the exact rational result on exact-arithmetic
+    inputs: a dropped, duplicated or misplaced outlier in the round trip
+    changes the sum."""
+    p = make_problem(2, 256, 128, frac=0.03, seed=31)
+    tc = oracle.pack_tile_coo(p.K, p.N, p.k, p.n, p.v, params)
+    Y = oracle.matmul_tile_coo(p.X, p.Wq, p.scales, p.zeros, p.K, p.N, p.group, tc)
+    q = oracle.codes(p.Wq, p.K, p.N)
+    xs = oracle.bf16_to_f64(p.X)
+    scales = oracle.f16_to_f64(p.scales)
+    vals = oracle.bf16_to_f64(p.v)
+    W = np.zeros((p.K, p.N))
+    for k in range(p.K):
+        for n in range(p.N):
+            zz = (int(p.zeros[k // p.group, n // 8]) >> (4 * (n % 8))) & 0xF
+            W[k, n] = scales[k // p.group, n] * (int(q[k, n]) - zz)
+    for a, b, c in zip(p.k, p.n, vals):
+        W[a, b] += c
+    for m in range(p.M):
+        for n in range(p.N):
+            ref = math.fsum(xs[m, k] * W[k, n] for k in range(p.K))
+            assert abs(Y[m, n] - ref) <= 1e-12 * (1 + abs(ref))
+    e = make_exact_problem(2, 256, 64, frac=0.05, seed=32)
+    te = oracle.pack_tile_coo(e.K, e.N, e.k, e.n, e.v, params)
+    Ye = oracle.matmul_tile_coo(e.X, e.Wq, e.scales, e.zeros, e.K, e.N, e.group, te)
+    assert np.array_equal(Ye, oracle.matmul(e.X, e.Wq, e.scales, e.zeros, e.K, e.N, e.group,
+                                            e.k, e.n, e.v))
+    # and a copy with one outlier dropped from the packed groups does not match
+    bad = oracle.TileCOO(te.params, te.tile_indptr, te.bucket_info, te.packed.copy(), te.nnz)
+    g = bad.packed.reshape(-1, 4)
+    real = np.argwhere((g[:, 2] & 0xFFFF) != 0)[0, 0]
+    g[real, 2] &= np.uint32(0xFFFF0000)
+    Yb = oracle.matmul_tile_coo(e.X, e.Wq, e.scales, e.zeros, e.K, e.N, e.group, bad)
+    assert not np.array_equal(Yb, Ye)

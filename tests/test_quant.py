@@ -151,14 +151,17 @@ def test_library_quantiser_matches_oracle(seed, frac):
         assert np.array_equal(a, b), name
 
 
-def test_library_padding_fill_matches_oracle():
+@pytest.mark.parametrize("buckets,group_mode", [(16, 0), (1, 1)],
+                         ids=["by_column_16", "by_bucket_1"])
+def test_library_padding_fill_matches_oracle(buckets, group_mode):
     fq = _fq()
     K, N = 512, 192
     W = make_dense_weight(K, N, seed=9)
     got = fq.fq_quantize_outlier_aware(W, 0.02)
     Wq, scales, zeros, k, n, v = quant.quantize(W, 0.02)
-    host = fq.fq_pack_tile_coo(K, N, got.k, got.n, got.v)
-    tc = oracle.pack_tile_coo(K, N, k, n, v)
+    host = fq.fq_pack_tile_coo(K, N, got.k, got.n, got.v,
+                               {"buckets_per_tile": buckets, "group_mode": group_mode})
+    tc = oracle.pack_tile_coo(K, N, k, n, v, oracle.Params(buckets=buckets, group_mode=group_mode))
     assert fq.fq_fill_padding_slots(W, got, host) == quant.fill_padding(W, 128, tc, Wq, zeros)
     assert np.array_equal(host.packed, np.asarray(tc.packed, np.uint32))
     assert np.array_equal(got.Wq, Wq)
