@@ -308,10 +308,13 @@ fq_status fq_workspace_bytes(const fq_problem* pr, size_t* bytes);
  *          with at most 16 rows per 32-row slab (ceil(M/4)), 6 or 8 with 17..24
  *          or 25..32 (not with outlier waves or Stream-K); the MFMA mapping
  *          only, else 0
+ *   cfg[9] 1 when each wave loads the scales and zero-points of all its tiles
+ *          (at most 16) at once, before its first tile, instead of with every
+ *          tile; else 0 (Stream-K, or more tiles per wave)
  * Errors: FQ_ERR_NULL, FQ_ERR_SHAPE, FQ_ERR_FORMAT (group_mode), FQ_ERR_UNSUPPORTED.
  */
 fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t group_mode,
-                           int32_t cfg[9]);
+                           int32_t cfg[10]);
 
 /*
  * fq_w4a16_outlier_matmul -- fused Y = X dequant(W_Q) + X W_O in one kernel

@@ -456,13 +456,13 @@ def fq_launch_config(M: int, K: int, N: int, split_k: int = 0, sparse: str = "au
         buckets_per_tile = d.buckets_per_tile if buckets_per_tile is None else buckets_per_tile
         group_mode = d.group_mode if group_mode is None else group_mode
     pr = _problem(M, K, N, FQ_Y_BF16, split_k, 128, sparse, flags)
-    cfg = (C.c_int32 * 9)()
+    cfg = (C.c_int32 * 10)()
     _check(lib.fq_launch_config(C.byref(pr), buckets_per_tile, group_mode, cfg),
            "fq_launch_config")
     return {"strip_cols": cfg[0], "split_k": cfg[1], "dense_waves": cfg[2],
             "outlier_waves": cfg[3], "mapping": "gather" if cfg[4] == FQ_SPARSE_GATHER else "mfma",
             "workgroups": cfg[5], "stream_k": bool(cfg[6]), "lds_bytes": cfg[7],
-            "x_staged": bool(cfg[8]), "x_stage_loads": cfg[8]}
+            "x_staged": bool(cfg[8]), "x_stage_loads": cfg[8], "bulk_scales": bool(cfg[9])}
 
 
 def fq_workspace_bytes(M: int, K: int, N: int, y_dtype=FQ_Y_BF16, split_k: int = 0,

@@ -24,10 +24,15 @@ HIP_SOURCES = ["kernels.hip"]
 
 # Packed-fp32 VALU forms are kept out of every HIP object.  MFMA results stay
 # in ordinary VGPRs (the accumulation registers would need a copy-out per
-# tile before the fp32 scale and zero-point step).
+# tile before the fp32 scale and zero-point step).  Kernel arguments are
+# preloaded into scalar registers.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+             # the hardware loads the first 14 kernel-argument dwords into
+             # scalar registers before a wave starts (no argument fetch on the
+             # path to a kernel's first loads)
+             "-mllvm", "-amdgpu-kernarg-preload-count=14",
              "-Wall", "-Wno-unused-result"]
 HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra"]
 

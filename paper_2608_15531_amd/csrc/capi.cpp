@@ -65,16 +65,20 @@ int plan_mode(const fq_problem* pr, int32_t group_mode) {
   return -1;
 }
 
+bool plan_for(const fq_problem* pr, const fq_tilecoo_dev* tc, bool dense, bool sparse,
+              fqi::Plan* plan) {
+  const int mode = plan_mode(pr, sparse ? tc->params.group_mode : FQ_GROUP_BY_COLUMN);
+  return fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, dense, sparse,
+                        sparse ? tc->params.buckets_per_tile : 0,
+                        sparse ? tc->max_tile_groups : 0, plan, mode, plan_opts(pr));
+}
+
 fq_status run(const fq_problem* pr, const uint16_t* X, const uint32_t* Wq,
               const uint16_t* scales, const uint32_t* zeros, const fq_tilecoo_dev* tc, void* Y,
               void* workspace, size_t workspace_bytes, void* stream, bool dense, bool sparse,
               const float* y_addend) {
   fqi::Plan plan;
-  const int mode = plan_mode(pr, sparse ? tc->params.group_mode : FQ_GROUP_BY_COLUMN);
-  if (!fqi::make_plan(pr->M, pr->K, pr->N, pr->split_k, dense, sparse,
-                      sparse ? tc->params.buckets_per_tile : 0,
-                      sparse ? tc->max_tile_groups : 0, &plan, mode, plan_opts(pr)))
-    return FQ_ERR_UNSUPPORTED;
+  if (!plan_for(pr, tc, dense, sparse, &plan)) return FQ_ERR_UNSUPPORTED;
   if (!workspace) return FQ_ERR_WORKSPACE;
   if (workspace_bytes < plan.ws_bytes || !aligned(workspace, 256)) return FQ_ERR_WORKSPACE;
   fqi::MatmulPtrs p{};
@@ -127,7 +131,7 @@ const char* fq_status_string(fq_status s) {
 }
 
 fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32_t group_mode,
-                           int32_t cfg[9]) {
+                           int32_t cfg[10]) {
   if (!cfg) return FQ_ERR_NULL;
   fq_status st = check_problem(pr);
   if (st != FQ_OK) return st;
@@ -146,6 +150,7 @@ fq_status fq_launch_config(const fq_problem* pr, int32_t buckets_per_tile, int32
   cfg[6] = pl.stream;
   cfg[7] = int32_t(pl.lds_bytes);
   cfg[8] = pl.XS;
+  cfg[9] = pl.BK;
   return FQ_OK;
 }
 

@@ -42,6 +42,7 @@ struct Plan {
   int C;             // partial-sum slots per strip (most contributors to one strip)
   int B;             // buckets per tile
   int XS;            // row-wise X loads per tile through the LDS stage: 0, or 1, 2, 4 (ceil(M/4))
+  int BK;            // 1: a dense wave loads the scales and zero-points of all its tiles at once
   // dynamic LDS layout, bytes: one slot per wave (X slice or B-operand
   // image), then the gather-mode sparse output buffers or the X stages
   size_t slot_bytes, off_shc, off_flag, off_trash, off_xs, lds_bytes;

@@ -62,15 +62,87 @@ namespace fqk {
 constexpr int kXRow = fqi::kXStride;   // LDS row stride of a staged X slice, elements
 constexpr int kGatherLimitM = fqi::kGatherLimitM;
 
-// Kernel arguments.  The first 64 bytes (one scalar-cache line) hold what
-// every wave needs before its first loads: the schedule and the dense
-// operand pointers.
+// The arguments every wave needs before its first loads -- the dense and
+// Tile-COO operand pointers, the shape and the grid -- are separate scalar
+// kernel parameters, which the hardware preloads into scalar registers (the
+// build preloads the first 14 argument dwords: five pointers and four
+// 32-bit values), so no wave waits on a kernel-argument fetch before its
+// first load.  The rest travels in ArgsTail, behind them.  Inside the kernel
+// everything is gathered into one MatmulArgs.
+struct ArgsTail {
+  int C;               // partial-sum slots per strip (most contributors to one strip)
+  int y_f32;
+  const uint4* packed;
+  int64_t n_groups;
+  const float* y_addend;
+  void* Y;
+  float* partials;
+  uint32_t* counters;
+};
+
+// GS packs the grid of one 32-row slab (G, bits 0..19) and the uniform split
+// (S, bits 20..30); the plan keeps both in range.
+constexpr int kGBits = 20;
+
+// Dynamic LDS layout of one workgroup, bytes: one slot per wave (the staged X
+// slice in gather mode, the outlier B-operand image in MFMA mode), then the
+// per-wave X stages or the gather-mode sparse output buffers, the split-K
+// flag and the trash word.  A function of the kernel's template parameters
+// and the slab's row count only; the planner (host) and the kernel (device)
+// both call it, so the kernel needs no layout argument.
+struct LdsLayout {
+  uint32_t slot_bytes, off_xs, off_shc, off_flag, off_trash, lds_bytes;
+};
+
+__host__ __device__ inline uint32_t align16(uint32_t x) { return (x + 15u) & ~15u; }
+
+__host__ __device__ inline LdsLayout lds_layout(int MODE, int NCB, int NW, int NWS, int XS,
+                                                bool sparse, int slab_M) {
+  LdsLayout L{};
+  L.slot_bytes = MODE == 0 ? align16(uint32_t(slab_M) * fqi::kXStride * 2)
+                           : (sparse ? uint32_t(fqi::kImageBytes) / 4 * NCB : 0u);
+  // slots: one per wave, or one per outlier wave under specialisation; the
+  // reduction buffer (one strip tile per wave) reuses them
+  const uint32_t n_slots = NWS > 0 ? NWS : NW;
+  const uint32_t red_bytes = uint32_t(NW + NWS) * uint32_t(slab_M) * (16u * NCB) * 4u;
+  // two 16-row blocks with an outlier image stage X in the image
+  const bool stage_in_image = XS >= 6 && sparse;
+  if (XS && !stage_in_image) {
+    // images, then an XS KB X stage per wave.  After the tile loop the
+    // reduction buffer reuses them, and the split-K flag sits at the head of
+    // wave 0's stage when the reduction buffer ends before it.  Each wave's
+    // trash word is the head of its own stage.
+    L.off_xs = n_slots * L.slot_bytes;
+    const uint32_t st = L.off_xs + uint32_t(NW + NWS) * 1024u * XS;
+    const uint32_t end = st > red_bytes ? st : red_bytes;
+    L.off_shc = end;
+    L.off_trash = L.off_xs;
+    if (red_bytes <= L.off_xs) {
+      L.off_flag = L.off_xs;
+      L.lds_bytes = end;
+    } else {
+      L.off_flag = align16(end);
+      L.lds_bytes = L.off_flag + 16;
+    }
+  } else {
+    const uint32_t slots = n_slots * L.slot_bytes;
+    L.off_shc = align16(slots > red_bytes ? slots : red_bytes);
+    const uint32_t shc_bytes =
+        (sparse && MODE == 0) ? uint32_t(NW) * uint32_t(slab_M) * fqi::kTileN * 4u : 0u;
+    L.off_flag = align16(L.off_shc + shc_bytes);
+    L.off_trash = L.off_flag + 16;
+    L.off_xs = L.off_trash;   // no X stages of their own
+    L.lds_bytes = L.off_trash + 16;
+  }
+  return L;
+}
+
 struct MatmulArgs {
   int M, K, N;
   int T, S;
   int G;               // workgroups per 32-row slab
   int n_slabs;         // 32-row slabs of M (grid = workgroups per slab x slabs)
-  int C;               // partial-sum slots per strip (most contributors to one strip)
+  int C;
   const uint32_t* Wq;
   const uint16_t* scales;
   const uint32_t* zeros;
@@ -79,10 +151,9 @@ struct MatmulArgs {
   const uint4* packed;
   int64_t n_groups;
   int y_f32;
-  int stream;          // 1: Stream-K ranges; 0: S uniform splits per strip
   int slot_bytes;      // one wave's LDS slot
   int off_shc;         // per-wave sparse output buffers (gather mode)
-  int off_flag;
+  int off_flag;        // split-K flag
   int off_trash;       // 16 bytes that padding slots are written to (MFMA mode)
   int off_xs;          // per-wave X stages (MFMA mode, one 16-row block)
   const float* y_addend;
@@ -91,14 +162,20 @@ struct MatmulArgs {
   uint32_t* counters;
 };
 
-static_assert(offsetof(MatmulArgs, X) + 8 <= 64 && offsetof(MatmulArgs, tile_indptr) == 64 &&
-                  offsetof(MatmulArgs, Y) >= 128 && sizeof(MatmulArgs) <= 192,
-              "argument lines: schedule and dense operands, sparse operands and LDS layout, output");
+// Tile-COO groups loaded with a tile, one per lane: at 1 % outliers a 128 x 64
+// tile holds about 21 groups in the default packing (47 by column), so one
+// 64-group load covers it; the rare larger tiles load the rest in the tile's
+// compute.  Every load instruction a tile issues costs time whatever its
+// size, so a tile issues as few as it can.
+constexpr int kGroupLoads = 1;
 
-// Global loads one tile costs in each mode (each counts once in vmcnt).
-template <int MB, int MODE, bool DENSE, bool SPARSE, int XR>
+// Global loads one tile costs in each mode (each counts once in vmcnt).  With
+// BK the scales and zero-points of all of a wave's tiles are loaded once,
+// before its first tile.
+template <int MB, int MODE, bool DENSE, bool SPARSE, int XR, bool BK>
 constexpr int loads_per_tile() {
-  return (DENSE ? 6 : 0) + (MODE == 0 ? 1 : XR > 0 ? XR : 4 * MB) + (SPARSE ? 2 : 0);
+  return (DENSE ? (BK ? 4 : 6) : 0) + (MODE == 0 ? 1 : XR > 0 ? XR : 4 * MB) +
+         (SPARSE ? kGroupLoads : 0);
 }
 
 // Tiles in flight per wave.  Each buffer is one more copy of the tile code
@@ -122,7 +199,7 @@ struct TileRegs {
   uint32_t z;      // zero-point word holding those columns
   uint4 x[NX];     // MODE 0: X chunk lane (row lane/16, elements 8*(lane%16)..+7)
                    // MODE 1: A fragment [mb][step]: row 16mb + c4, elements 32step + 8h..+7
-  uint4 g[2];      // Tile-COO groups lane and lane + 64 of the tile
+  uint4 g[kGroupLoads];   // Tile-COO group lane (+ 64 j) of the tile
   uint32_t g0, g1; // the tile's group range
 };
 
@@ -173,7 +250,7 @@ struct Operands {
 // counts outstanding loads exactly across the prefetch.  A wave-wide load of
 // one step covers 4 packed rows x (16 NCB) columns: 128-byte row segments for
 // 32-column strips, 256-byte ones for 64-column strips.
-template <int MB, int MODE, int NCB, bool DENSE, int XR>
+template <int MB, int MODE, int NCB, bool DENSE, int XR, bool BK>
 __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Operands<MB>& op,
                                                 int t, int n0, TileRegs<MB, MODE, NCB>& r) {
   if (DENSE) {
@@ -183,13 +260,13 @@ __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Opera
     if constexpr (NCB == 4) {
 #pragma unroll
       for (int step = 0; step < 4; ++step) r.w[step] = buf_load16(op.w, op.lw, wt + step * step_bytes);
-      r.s = buf_load8(op.s, op.ls, st);
+      if (!BK) r.s = buf_load8(op.s, op.ls, st);
     } else {
 #pragma unroll
       for (int step = 0; step < 4; ++step) r.w[step] = buf_load8(op.w, op.lw, wt + step * step_bytes);
-      r.s = buf_load4(op.s, op.ls, st);
+      if (!BK) r.s = buf_load4(op.s, op.ls, st);
     }
-    r.z = buf_load4(op.z, op.lz, (uint32_t(t) * uint32_t(a.N >> 3) + uint32_t(n0 >> 3)) * 4u);
+    if (!BK) r.z = buf_load4(op.z, op.lz, (uint32_t(t) * uint32_t(a.N >> 3) + uint32_t(n0 >> 3)) * 4u);
   }
   const uint32_t xt = uint32_t(t) * 256u;
   if (MODE == 0) {
@@ -205,7 +282,7 @@ __device__ __forceinline__ void load_tile_dense(const MatmulArgs& a, const Opera
   }
 }
 
-// The tile's first two Tile-COO groups, one per lane and half-wave pass.
+// The tile's first 64 kGroupLoads Tile-COO groups, one per lane and pass.
 template <int MB, int MODE, int NCB, bool SPARSE>
 __device__ __forceinline__ void load_tile_sparse(const Operands<MB>& op, int lane, uint32_t g0,
                                                  uint32_t g1, TileRegs<MB, MODE, NCB>& r) {
@@ -217,8 +294,74 @@ __device__ __forceinline__ void load_tile_sparse(const Operands<MB>& op, int lan
     // with no outliers at all `packed` points at valid scratch.
     const uint32_t last = g1 > g0 ? g1 - 1 - g0 : 0u;
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < kGroupLoads; ++j)
       r.g[j] = buf_load16(op.g, min(uint32_t(lane + 64 * j), last) * 16u, g0 * 16u);
+  }
+}
+
+// With BK, the fp16 scales and INT4 zero-points of up to kBulkTiles of a
+// wave's tiles, loaded once before its first tile with a few loads whose
+// lanes each take one tile's share, and handed to the lanes that need them
+// with ds_bpermute when the tile is computed.
+//   64-column strips: scales bs[j], lane 16 tt' + c holds the 4 scales of
+//   columns 4c..4c+3 of tile w_lo + 4 j + tt' (8 bytes); zero-points bz[j],
+//   lane 8 tt' + q holds word q (columns 8q..8q+7) of tile w_lo + 8 j + tt'.
+//   32-column strips: scales, lane 16 tt' + c holds columns 2c, 2c+1 (4
+//   bytes) of tile w_lo + 4 j + tt'; zero-points, lane 4 tt + q holds word q
+//   of tile w_lo + tt.
+constexpr int kBulkTiles = 16;
+
+template <int NCB>
+struct BulkRegs {
+  typename StripVec<NCB>::scales s[4];
+  uint32_t z[NCB == 4 ? 2 : 1];
+};
+
+template <int MB, int NCB>
+__device__ __forceinline__ void load_bulk(const MatmulArgs& a, const Operands<MB>& op, int w_lo,
+                                          int w_hi, int n0, int lane, BulkRegs<NCB>& b) {
+  const int last = w_hi - 1;   // lanes past the wave's last tile reload it
+  const uint32_t N = uint32_t(a.N);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t t = uint32_t(min(w_lo + 4 * j + (lane >> 4), last));
+    const uint32_t off = (t * N + uint32_t(n0) + uint32_t(NCB * (lane & 15))) * 2u;
+    if constexpr (NCB == 4) b.s[j] = buf_load8(op.s, off, 0u);
+    else b.s[j] = buf_load4(op.s, off, 0u);
+  }
+  constexpr int TPZ = NCB == 4 ? 8 : 16;   // tiles per zero-point load
+  constexpr int WPT = 2 * NCB;   // zero-point words per tile row of the strip (8 columns each)
+  static_assert(WPT * TPZ == 64, "one zero-point word per lane");
+#pragma unroll
+  for (int j = 0; j < (NCB == 4 ? 2 : 1); ++j) {
+    const uint32_t t = uint32_t(min(w_lo + TPZ * j + lane / WPT, last));
+    const uint32_t off = (t * (N >> 3) + uint32_t(n0 >> 3) + uint32_t(lane % WPT)) * 4u;
+    b.z[j] = buf_load4(op.z, off, 0u);
+  }
+}
+
+// The scales and zero-point word of tile w_lo + tt for lane c, by bpermute
+// from the lane that loaded them.  Tiles are computed in order, and the bulk
+// registers are shifted down after every 4th (scales) and 8th (zero-points)
+// tile, so the current ones are always element 0 (a register array indexed by
+// a run-time tile number would be placed in scratch memory).
+template <int NCB>
+__device__ __forceinline__ void bulk_tile(BulkRegs<NCB>& b, int tt, int c,
+                                          typename StripVec<NCB>::scales& s, uint32_t& z) {
+  const int sl = (16 * (tt & 3) + c) * 4;
+  if constexpr (NCB == 4) {
+    s.x = uint32_t(__builtin_amdgcn_ds_bpermute(sl, int(b.s[0].x)));
+    s.y = uint32_t(__builtin_amdgcn_ds_bpermute(sl, int(b.s[0].y)));
+    z = uint32_t(__builtin_amdgcn_ds_bpermute((8 * (tt & 7) + (c >> 1)) * 4, int(b.z[0])));
+    if ((tt & 7) == 7) b.z[0] = b.z[1];
+  } else {
+    s = uint32_t(__builtin_amdgcn_ds_bpermute(sl, int(b.s[0])));
+    z = uint32_t(__builtin_amdgcn_ds_bpermute((4 * tt + (c >> 2)) * 4, int(b.z[0])));
+  }
+  if ((tt & 3) == 3) {
+    b.s[0] = b.s[1];
+    b.s[1] = b.s[2];
+    b.s[2] = b.s[3];
   }
 }
 
@@ -390,9 +533,11 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
 // Two 16-row blocks hold the most registers; they are kept to two waves per
 // SIMD (half the register file), which every instance launched fits without
 // spilling.
-template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS, int XR>
+template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS, int XR, bool BK>
 __global__ void __launch_bounds__(64 * (NW + NWS))
-    __attribute__((amdgpu_waves_per_eu(MB == 2 ? 2 : 1))) matmul_kernel(MatmulArgs args) {
+    __attribute__((amdgpu_waves_per_eu(MB == 2 ? 2 : 1))) matmul_kernel(
+        const uint32_t* Wq, const uint16_t* scales, const uint32_t* zeros, const uint16_t* X,
+        const uint32_t* tile_indptr, int M, int K, int N, int GS, ArgsTail tail) {
   static_assert(NCB == 4 || (NCB == 2 && MODE == 1), "32-column strips use the MFMA outlier mapping");
   static_assert(XR == 0 || ((XR == 1 || XR == 2 || XR == 4) && MODE == 1 && MB == 1) ||
                     ((XR == 6 || XR == 8) && MODE == 1 && MB == 2 && NWS == 0),
@@ -402,6 +547,7 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
   constexpr int NT = NW + NWS;                 // waves per workgroup
   constexpr bool WS = NWS > 0;
   static_assert(!WS || (KD && KS && MODE == 1 && !SK), "outlier waves: fused MFMA mapping, split-K");
+  static_assert(!BK || (KD && !SK), "bulk scale loads: dense waves, uniform split-K");
   constexpr int NC = 16 * NCB;                 // strip width, columns
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
@@ -412,12 +558,33 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
   const int h = lane >> 4;                     // k-chunk of the MFMA operands
   const int c4 = lane & 15;                    // MFMA column / A row
 
-  // The arguments span three 64-byte scalar-cache lines.  One field of each is
-  // requested here, before anything waits on the first, so that a wave pays
-  // one memory round trip for all of them: otherwise the second line costs a
-  // round trip before the first tile's loads and the third one in the
-  // epilogue.
-  asm volatile("" ::"s"(args.G), "s"(args.tile_indptr), "s"(args.Y));
+  // The tail's scalar loads are issued at entry and first waited on where a
+  // tail field is used, after the first operand loads are out.
+  // Narrow (32-column) and gather instances hold more scalar state: their
+  // compiler-scheduled tail loads would otherwise be split over two waited
+  // round trips before the first loads, so they take the whole tail in one.
+  if constexpr (NCB == 2 || MODE == 0) asm volatile("" ::"s"(tail.packed), "s"(tail.Y));
+  MatmulArgs args;
+  args.M = M;
+  args.K = K;
+  args.N = N;
+  args.T = K >> 7;                          // 128-row tiles
+  args.G = GS & ((1 << kGBits) - 1);
+  args.S = GS >> kGBits;
+  args.n_slabs = (M + fqi::kSlabM - 1) / fqi::kSlabM;
+  args.Wq = Wq;
+  args.scales = scales;
+  args.zeros = zeros;
+  args.X = X;
+  args.tile_indptr = tile_indptr;
+  {
+    const LdsLayout L = lds_layout(MODE, NCB, NW, NWS, XR, KS, min(M, fqi::kSlabM));
+    args.slot_bytes = int(L.slot_bytes);
+    args.off_shc = int(L.off_shc);
+    args.off_flag = int(L.off_flag);
+    args.off_trash = int(L.off_trash);
+    args.off_xs = int(L.off_xs);
+  }
 
   // Work: the units (strip, tile) of each 32-row slab, strip-major
   // (u = strip * T + tile, which is also the Tile-COO tile index).  A
@@ -450,10 +617,8 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
   const int n_strips = args.N / NC;
   a.M = min(fqi::kSlabM, args.M - m0);
   a.X = args.X + size_t(m0) * args.K;
-  a.Y = static_cast<char*>(args.Y) + size_t(m0) * args.N * (args.y_f32 ? 4 : 2);
-  if (args.y_addend) a.y_addend = args.y_addend + size_t(m0) * args.N;
-  a.partials = args.partials + size_t(slab) * n_strips * args.C * fqi::kSlabM * NC;
-  a.counters = args.counters + size_t(slab) * n_strips;
+  // (the output-side pointers of the slab are set after the tile loop: they
+  // come from the argument tail, which nothing before the first loads waits on)
   // Uniform split-K: workgroup wg is K range sp of strip st (32-bit math;
   // no division at all without a split).  Stream-K: an even share of the
   // U = strips x tiles units, as 64-bit ranges.
@@ -490,7 +655,6 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
   op.s = make_rsrc(a.scales, uint32_t(a.K / 128) * uint32_t(a.N) * 2u);
   op.z = make_rsrc(a.zeros, uint32_t(a.K / 128) * uint32_t(a.N / 8) * 4u);
   op.x = make_rsrc(a.X, uint32_t(a.M) * uint32_t(a.K) * 2u);
-  op.g = make_rsrc(a.packed, uint32_t(max(a.n_groups, int64_t(1))) * 16u);
   op.lw = uint32_t(h * a.N + NCB * c4) * 4u;
   op.ls = uint32_t(c4) * (2u * NCB);
   op.lz = uint32_t((NCB * c4) >> 3) * 4u;
@@ -526,6 +690,7 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
   int64_t tile_base = 0;
   uint32_t tp = 0;
   f32x4_t acc[MB][NCB];
+  BulkRegs<NCB> bulk;   // BK: scales and zero-points of the wave's tiles
 
   // The tile pipeline of one wave for one role: dense and outlier work
   // (every wave without specialisation), or one of them.
@@ -542,11 +707,11 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       load_tile_sparse<MB, MODE, NCB, SPARSE>(op, lane, g0, g1, r);
     };
     auto issue = [&](int t, TileRegs<MB, MODE, NCB>& r) __attribute__((always_inline)) {
-      load_tile_dense<MB, MODE, NCB, DENSE, XR>(a, op, t, n0, r);
+      load_tile_dense<MB, MODE, NCB, DENSE, XR, BK>(a, op, t, n0, r);
       issue_sparse(t, r);
     };
 
-    auto compute = [&](const TileRegs<MB, MODE, NCB>& cur) __attribute__((always_inline)) {
+    auto compute = [&](const TileRegs<MB, MODE, NCB>& cur, int tt) __attribute__((always_inline)) {
       // ---- X fragments
       bf16x8_t A[MB][4];
       if (MODE == 0) {
@@ -640,19 +805,22 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       // 4h + r with r >= M (M < 4) never reach the output: skip them.
       if (DENSE) {
         float sc[NCB], zf[NCB];
+        typename StripVec<NCB>::scales cs = cur.s;
+        uint32_t cz = cur.z;
+        if constexpr (BK) bulk_tile<NCB>(bulk, tt, c4, cs, cz);
         if constexpr (NCB == 4) {
-          sc[0] = f16_bits_to_f32(cur.s.x & 0xFFFFu);
-          sc[1] = f16_bits_to_f32(cur.s.x >> 16);
-          sc[2] = f16_bits_to_f32(cur.s.y & 0xFFFFu);
-          sc[3] = f16_bits_to_f32(cur.s.y >> 16);
+          sc[0] = f16_bits_to_f32(cs.x & 0xFFFFu);
+          sc[1] = f16_bits_to_f32(cs.x >> 16);
+          sc[2] = f16_bits_to_f32(cs.y & 0xFFFFu);
+          sc[3] = f16_bits_to_f32(cs.y >> 16);
         } else {
-          sc[0] = f16_bits_to_f32(cur.s & 0xFFFFu);
-          sc[1] = f16_bits_to_f32(cur.s >> 16);
+          sc[0] = f16_bits_to_f32(cs & 0xFFFFu);
+          sc[1] = f16_bits_to_f32(cs >> 16);
         }
         // the lane's columns n0 + NCB*c4 + c sit at nibbles (NCB*c4) % 8 + c of the word
         const int zsh = ((NCB * c4) & 7) * 4;
   #pragma unroll
-        for (int c = 0; c < NCB; ++c) zf[c] = kCodeOffset + float((cur.z >> (zsh + 4 * c)) & 15u);
+        for (int c = 0; c < NCB; ++c) zf[c] = kCodeOffset + float((cz >> (zsh + 4 * c)) & 15u);
   #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
   #pragma unroll
@@ -672,12 +840,12 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       // is skipped -- a wave-uniform branch, no per-lane masking.
       uint32_t n_g = 0;
       if (SPARSE) n_g = cur.g1 - cur.g0;
-      uint32_t addr[2][4];
+      uint32_t addr[kGroupLoads][4];
       if (SPM) {
   #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < kGroupLoads; ++j)
           if (n_g > 64u * j) scatter_group<NCB>(img, trash, cur.g[j], half, addr[j]);
-        for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
+        for (uint32_t gi = 64 * kGroupLoads + lane; gi < n_g; gi += 64) {
           uint32_t ad[4];
           scatter_group<NCB>(img, trash, a.packed[cur.g0 + gi], half, ad);
         }
@@ -697,11 +865,11 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       }
 
       // ---- gather mapping: the first two groups' X values from the staged slice
-      Gathered gx[2];
-      bool gsingle[2] = {false, false};
+      Gathered gx[kGroupLoads];
+      bool gsingle[kGroupLoads] = {};
       if (SPARSE && MODE == 0) {
   #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < kGroupLoads; ++j) {
           gsingle[j] = uint32_t(lane + 64 * j) < n_g && single_column(decode_group(cur.g[j]));
           if (gsingle[j]) gather_x(a, xs, cur.g[j], gx[j]);
         }
@@ -711,9 +879,9 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       if (SPM) {
         __builtin_amdgcn_wave_barrier();
   #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < kGroupLoads; ++j)
           if (n_g > 64u * j) clear_group(addr[j]);
-        for (uint32_t gi = 128 + lane; gi < n_g; gi += 64) {
+        for (uint32_t gi = 64 * kGroupLoads + lane; gi < n_g; gi += 64) {
           uint32_t o01, o23;
           const uint4 raw = a.packed[cur.g0 + gi];
           image_offsets<NCB>(raw.x, raw.y, o01, o23);
@@ -725,11 +893,11 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       // ---- gather mapping: finish the first two groups, then any further ones
       if (SPARSE && MODE == 0) {
   #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < kGroupLoads; ++j) {
           if (gsingle[j]) gather_add(a, cur.g[j], gx[j], shc);
           else if (uint32_t(lane + 64 * j) < n_g) sparse_gather(a, xs, cur.g[j], shc);
         }
-        for (uint32_t gi = 128 + lane; gi < n_g; gi += 64)
+        for (uint32_t gi = 64 * kGroupLoads + lane; gi < n_g; gi += 64)
           sparse_gather(a, xs, a.packed[cur.g0 + gi], shc);
       }
       __builtin_amdgcn_wave_barrier();
@@ -746,14 +914,33 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
     // tile_indptr, while its dense loads are already out.
     // The loop body holds one copy of the tile code per register buffer; the
     // last partial round is predicated, not peeled.
-    constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE, XR>();
+    constexpr int NL = loads_per_tile<MB, MODE, DENSE, SPARSE, XR, BK && DENSE>();
     constexpr int D = pipeline_depth<MB, NCB>();
     TileRegs<MB, MODE, NCB> rg[D];
     if (w_lo < w_hi) {
       const int last = w_hi - 1;
+      // With BK the scales and zero-points of every tile of the wave go out
+      // first (the first tile's epilogue needs them), then the first D
+      // tiles' dense loads; their group loads wait for tile_indptr (and the
+      // Tile-COO descriptor from the argument tail), and follow.  From then
+      // on every tile issues dense, then groups.
+      if constexpr (BK && DENSE) {
+        load_bulk<MB, NCB>(a, op, w_lo, w_hi, n0, lane, bulk);
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
       for (int i = 0; i < D; ++i) {
-        issue(min(w_lo + i, last), rg[i]);
+        load_tile_dense<MB, MODE, NCB, DENSE, XR, BK>(a, op, min(w_lo + i, last), n0, rg[i]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (SPARSE) {
+        a.packed = tail.packed;
+        a.n_groups = tail.n_groups;
+        op.g = make_rsrc(a.packed, uint32_t(max(a.n_groups, int64_t(1))) * 16u);
+      }
+#pragma unroll
+      for (int i = 0; i < D; ++i) {
+        issue_sparse(min(w_lo + i, last), rg[i]);
         __builtin_amdgcn_sched_barrier(0);
       }
       for (int t = w_lo; t < w_hi; t += D) {
@@ -761,7 +948,7 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
         for (int i = 0; i < D; ++i) {
           if (i == 0 || t + i < w_hi) {
             wait_vmcnt<(D - 1) * NL>();
-            compute(rg[i]);
+            compute(rg[i], t + i - w_lo);
           }
           issue(min(t + i + D, last), rg[i]);
           __builtin_amdgcn_sched_barrier(0);
@@ -773,9 +960,6 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
   // Partial sums cross workgroups through device-coherent (sc1) 16-byte
   // accesses, the encoding of relaxed agent-scope atomics; no cache-wide
   // writeback or invalidate is issued.
-  const __amdgpu_buffer_rsrc_t prs =
-      make_rsrc(a.partials, uint32_t(n_strips) * uint32_t(a.C) * uint32_t(a.M) * (4u * NC));
-
   for (int64_t u = u_begin;;) {
     // ------------------------------------------------------------ segment
     // this workgroup's tiles [t_lo, t_hi) of the strip, the number of
@@ -843,6 +1027,26 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       tiles(std::integral_constant<bool, KD>{}, std::integral_constant<bool, KS>{});
     }
     __syncthreads();
+
+    // Output side of this slab, from the argument tail.
+    {
+      int t_C = tail.C, t_f32 = tail.y_f32;
+      const float* t_add = tail.y_addend;
+      void* t_Y = tail.Y;
+      float* t_part = tail.partials;
+      uint32_t* t_cnt = tail.counters;
+      // the first use of the tail's output-side fields: the compiler may not
+      // hoist their arithmetic (and the wait for them) above this point
+      asm volatile("" : "+s"(t_C), "+s"(t_f32), "+s"(t_add), "+s"(t_Y), "+s"(t_part), "+s"(t_cnt));
+      a.C = t_C;
+      a.y_f32 = t_f32;
+      a.Y = static_cast<char*>(t_Y) + size_t(m0) * args.N * (t_f32 ? 4 : 2);
+      a.y_addend = t_add ? t_add + size_t(m0) * args.N : nullptr;
+      a.partials = t_part + size_t(slab) * n_strips * t_C * fqi::kSlabM * NC;
+      a.counters = t_cnt + size_t(slab) * n_strips;
+    }
+    const __amdgpu_buffer_rsrc_t prs =
+        make_rsrc(a.partials, uint32_t(n_strips) * uint32_t(a.C) * uint32_t(a.M) * (4u * NC));
 
     // -------------------------------------------------------------- reduce
 #pragma unroll
@@ -951,29 +1155,54 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
   }
 }
 
-template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK, int NWS, int XR>
+template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK, int NWS, int XR,
+          bool BK>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR>;
-  if (pl.lds_bytes > 65536) {
+  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR, BK>;
+  // the layout of this instance (with no outliers the fused launch drops its
+  // sparse half, whose layout is never larger than the plan's)
+  const uint32_t lds = lds_layout(MODE, NCB, NW, NWS, XR, SPARSE, pl.slab_M).lds_bytes;
+  if (lds > 160u * 1024u) return int(hipErrorInvalidValue);
+  if (lds > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(pl.lds_bytes));
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return int(e);
   }
   const unsigned grid = unsigned(pl.G) * unsigned(pl.n_slabs);
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * (NW + NWS)), pl.lds_bytes, stream, args);
+  ArgsTail tail;
+  tail.C = args.C;
+  tail.y_f32 = args.y_f32;
+  tail.packed = args.packed;
+  tail.n_groups = args.n_groups;
+  tail.y_addend = args.y_addend;
+  tail.Y = args.Y;
+  tail.partials = args.partials;
+  tail.counters = args.counters;
+  const int GS = args.G | (args.S << kGBits);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * (NW + NWS)), lds, stream, args.Wq,
+                     args.scales, args.zeros, args.X, args.tile_indptr, args.M, args.K, args.N, GS,
+                     tail);
   return int(hipGetLastError());
+}
+
+template <int MB, int MODE, int NCB, int NW, bool SK, int XR, bool BK>
+int launch_roles_bk(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse,
+                    hipStream_t s) {
+  if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8) && XR < 6) {
+    if (dense && sparse && pl.NWS > 0)
+      return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2, XR, BK>(pl, a, s);
+  }
+  if (dense && sparse) return launch_variant<MB, MODE, NCB, true, true, NW, SK, 0, XR, BK>(pl, a, s);
+  if (dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK, 0, XR, BK>(pl, a, s);
+  return launch_variant<MB, MODE, NCB, false, true, NW, SK, 0, XR, false>(pl, a, s);
 }
 
 template <int MB, int MODE, int NCB, int NW, bool SK, int XR>
 int launch_roles(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse, hipStream_t s) {
-  if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8) && XR < 6) {
-    if (dense && sparse && pl.NWS > 0)
-      return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2, XR>(pl, a, s);
+  if constexpr (!SK) {
+    if (pl.BK && dense) return launch_roles_bk<MB, MODE, NCB, NW, SK, XR, true>(pl, a, dense, sparse, s);
   }
-  if (dense && sparse) return launch_variant<MB, MODE, NCB, true, true, NW, SK, 0, XR>(pl, a, s);
-  if (dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK, 0, XR>(pl, a, s);
-  return launch_variant<MB, MODE, NCB, false, true, NW, SK, 0, XR>(pl, a, s);
+  return launch_roles_bk<MB, MODE, NCB, NW, SK, XR, false>(pl, a, dense, sparse, s);
 }
 
 template <int MB, int MODE, int NCB, int NW, bool SK>
@@ -1205,49 +1434,26 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
     p.C = p.S;
   }
 
-  if (p.MODE == 0) {
-    p.slot_bytes = align_up(size_t(p.slab_M) * kXStride * 2, 16);
-  } else {
-    // 4 NCB B-operand blocks of 64 x 16 B
-    p.slot_bytes = sparse ? size_t(kImageBytes) / 4 * p.NCB : 0;
-  }
-  // slots: one per wave, or one per outlier wave under specialisation; the
-  // reduction buffer (one tile per wave) reuses them
-  const int n_slots = p.NWS > 0 ? p.NWS : p.NW;
-  const size_t red_bytes = size_t(p.NW + p.NWS) * p.slab_M * (16 * p.NCB) * 4;
   // X staging with the MFMA mapping: ceil(M / 4) row-wise loads per tile
   // (1, 2 or 4) for one 16-row block, 6 or 8 for two (not beside outlier waves,
   // whose dense waves have no image to stage in, nor under Stream-K, whose
   // two-block kernels would spill registers)
   p.XS = (p.MODE == 1 && p.MB == 1) ? (p.slab_M <= 4 ? 1 : p.slab_M <= 8 ? 2 : 4)
          : (p.MODE == 1 && p.MB == 2 && p.NWS == 0 && !p.stream) ? (p.slab_M <= 24 ? 6 : 8) : 0;
-  // two blocks with an outlier image stage in the image: no LDS of their own
-  const bool stage_in_image = p.XS >= 6 && sparse;
-  if (p.XS && !stage_in_image) {
-    // images, then an XS KB X stage per wave.  After the tile loop the
-    // reduction buffer reuses them, and the split-K flag sits at the head of
-    // wave 0's stage when the reduction buffer ends before it.  Each wave's
-    // trash word is the head of its own stage.
-    p.off_xs = n_slots * p.slot_bytes;
-    const size_t end = std::max(p.off_xs + size_t(p.NW + p.NWS) * 1024 * p.XS, red_bytes);
-    p.off_shc = end;
-    p.off_trash = p.off_xs;
-    if (red_bytes <= p.off_xs) {
-      p.off_flag = p.off_xs;
-      p.lds_bytes = end;
-    } else {
-      p.off_flag = align_up(end, 16);
-      p.lds_bytes = p.off_flag + 16;
-    }
-  } else {
-    p.off_shc = align_up(std::max(n_slots * p.slot_bytes, red_bytes), 16);
-    const size_t shc_bytes = (sparse && p.MODE == 0) ? size_t(p.NW) * p.slab_M * kTileN * 4 : 0;
-    p.off_flag = align_up(p.off_shc + shc_bytes, 16);
-    p.off_trash = p.off_flag + 16;
-    p.off_xs = p.off_trash;   // no X stages of their own
-    p.lds_bytes = p.off_trash + 16;
-  }
+  // scales and zero-points once per wave (uniform split-K, at most
+  // kBulkTiles tiles per dense wave)
+  p.BK = dense && !p.stream &&
+         ((p.T + p.S - 1) / p.S + p.NW - 1) / p.NW <= fqk::kBulkTiles;
+  const fqk::LdsLayout L = fqk::lds_layout(p.MODE, p.NCB, p.NW, p.NWS, p.XS, sparse, p.slab_M);
+  p.slot_bytes = L.slot_bytes;
+  p.off_xs = L.off_xs;
+  p.off_shc = L.off_shc;
+  p.off_flag = L.off_flag;
+  p.off_trash = L.off_trash;
+  p.lds_bytes = L.lds_bytes;
   if (p.lds_bytes > 160 * 1024) return false;
+  // the grid of one slab and the split travel packed in one kernel argument
+  if (p.G >= (1 << fqk::kGBits) || p.S >= (1 << (31 - fqk::kGBits))) return false;
 
   // partial sums: [slab][strip][slot][row][strip width] fp32, every slab kSlabM rows apart
   p.partial_bytes = p.C > 1 ? size_t(p.n_slabs) * p.n_strips * p.C * kSlabM * (16 * p.NCB) * 4 : 0;
@@ -1280,14 +1486,8 @@ int launch_matmul(const Plan& pl, const MatmulPtrs& p, bool dense, bool sparse, 
   a.T = pl.T;
   a.S = pl.S;
   a.G = pl.G;
-  a.stream = pl.stream;
   a.C = pl.C;
   a.n_slabs = pl.n_slabs;
-  a.slot_bytes = int(pl.slot_bytes);
-  a.off_shc = int(pl.off_shc);
-  a.off_flag = int(pl.off_flag);
-  a.off_trash = int(pl.off_trash);
-  a.off_xs = int(pl.off_xs);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (sparse && p.n_groups == 0) {
     // No outliers: the fused launch drops its sparse half; a sparse-only

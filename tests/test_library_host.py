@@ -70,7 +70,7 @@ def test_default_params(lib):
 
 def test_status_strings(lib):
     for s in range(11):
-        assert fq.fq_status_string(s)
+        assert fq.fq_status_string(s) and fq.fq_status_string(s) != "unknown status"
     assert fq.fq_status_string(0) == "ok"
 
 
