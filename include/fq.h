@@ -51,7 +51,9 @@ typedef enum {
   FQ_ERR_UNSUPPORTED = 7,  /* valid input the kernels do not implement */
   FQ_ERR_WORKSPACE = 8,    /* workspace missing or too small */
   FQ_ERR_HIP = 9,          /* the HIP runtime reported an error at launch */
-  FQ_ERR_ALIGN = 10        /* a device pointer is not aligned as required */
+  FQ_ERR_ALIGN = 10,       /* a device pointer is not aligned as required */
+  FQ_ERR_SCRATCH_LIMIT = 11  /* the allocation-free entry point's problem needs more
+                                scratch than its static maximum */
 } fq_status;
 
 /* Tile-COO grouping of outliers into 16-byte groups of four slots. */
@@ -338,6 +340,33 @@ fq_status fq_w4a16_outlier_matmul(const fq_problem* pr, const uint16_t* X, const
                                   const uint16_t* scales, const uint32_t* zeros,
                                   const fq_tilecoo_dev* tc, void* Y, void* workspace,
                                   size_t workspace_bytes, void* stream);
+
+/*
+ * fq_w4a16_outlier_matmul_noalloc -- fq_w4a16_outlier_matmul without a
+ * workspace argument and without any device allocation, for callers that
+ * cannot allocate: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments (minus the workspace),
+ * same kernels, same launch plan and the same result bit for bit.
+ * The workspace is a static device array of the library, FQ_NOALLOC_SCRATCH_BYTES
+ * (256 KiB of arrival counters plus 8 MiB of split-K partial sums), one copy per
+ * device, held until the process ends.  A problem whose launch plan needs
+ * more workspace than that returns FQ_ERR_SCRATCH_LIMIT before anything
+ * touches the device; every problem whose fq_workspace_bytes() is at most
+ * FQ_NOALLOC_SCRATCH_BYTES fits.  The first call on a device (with that device
+ * current) looks up the array's device address and clears its counters with
+ * one small kernel on `stream`, ahead of the matmul; every completed call
+ * leaves the counters at zero again.
+ * All calls on one device share its array: calls that may overlap in time on
+ * one device (different streams, concurrent graphs) race and give unspecified
+ * results; order them, or use fq_w4a16_outlier_matmul with separate workspaces.
+ * Errors: those of fq_w4a16_outlier_matmul (FQ_ERR_WORKSPACE aside),
+ * FQ_ERR_SCRATCH_LIMIT, FQ_ERR_HIP (also when the set-up fails).
+ */
+#define FQ_NOALLOC_SCRATCH_BYTES ((size_t)(256 * 1024 + (8 << 20)))
+fq_status fq_w4a16_outlier_matmul_noalloc(const fq_problem* pr, const uint16_t* X,
+                                          const uint32_t* Wq, const uint16_t* scales,
+                                          const uint32_t* zeros, const fq_tilecoo_dev* tc,
+                                          void* Y, void* stream);
 
 /*
  * fq_w4a16_outlier_matmul_unfused -- the same result with the two paths in

@@ -23,7 +23,9 @@ FQ_OK = 0
 STATUS_NAMES = {0: "FQ_OK", 1: "FQ_ERR_NULL", 2: "FQ_ERR_SHAPE", 3: "FQ_ERR_RANGE",
                 4: "FQ_ERR_DUPLICATE", 5: "FQ_ERR_ZERO_VALUE", 6: "FQ_ERR_FORMAT",
                 7: "FQ_ERR_UNSUPPORTED", 8: "FQ_ERR_WORKSPACE", 9: "FQ_ERR_HIP",
-                10: "FQ_ERR_ALIGN"}
+                10: "FQ_ERR_ALIGN", 11: "FQ_ERR_SCRATCH_LIMIT"}
+# static device scratch of fq_w4a16_outlier_matmul_noalloc (FQ_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 256 * 1024 + (8 << 20)
 FQ_GROUP_BY_COLUMN = 0
 FQ_GROUP_BY_BUCKET = 1
 FQ_REORDER_COLUMNS = 1
@@ -98,6 +100,8 @@ _SIGS = {
     "fq_w4a16_outlier_matmul_unfused": ([C.POINTER(fq_problem), _P, _P, _P, _P,
                                          C.POINTER(fq_tilecoo_dev), _P, _P, C.c_size_t, _P],
                                         C.c_int),
+    "fq_w4a16_outlier_matmul_noalloc": ([C.POINTER(fq_problem), _P, _P, _P, _P,
+                                         C.POINTER(fq_tilecoo_dev), _P, _P], C.c_int),
     "fq_w4a16_matmul": ([C.POINTER(fq_problem), _P, _P, _P, _P, _P, _P, C.c_size_t, _P],
                         C.c_int),
     "fq_debug_decode_tile_coo": ([C.POINTER(fq_tilecoo_dev), C.c_int32, C.c_int32, _P, _P, _P,
@@ -383,6 +387,26 @@ def fq_w4a16_outlier_matmul(X, Wq, scales, zeros, tc: TileCOODevice, Y=None, y_d
                                        scales.data_ptr(), zeros.data_ptr(), C.byref(tcs),
                                        Y.data_ptr(), ws.data_ptr(), ws.numel(), sh),
            "fq_w4a16_outlier_matmul")
+    return Y
+
+
+def fq_w4a16_outlier_matmul_noalloc(X, Wq, scales, zeros, tc: TileCOODevice, Y,
+                                    y_dtype="bf16", split_k: int = 0, stream=None,
+                                    group: int = 128, sparse: str = "auto", flags: int = 0):
+    """Fused Y = X dequant(W_Q) + X W_O without a workspace: the library's
+    static device scratch serves as one.  Y is the caller's output tensor
+    (nothing is allocated here either); returns Y."""
+    lib = load()
+    if Y is None:
+        raise ValueError("fq_w4a16_outlier_matmul_noalloc: pass the output tensor Y")
+    M, K, N, ydt, Y = _matmul_args(X, Wq, scales, zeros, Y, y_dtype, group)
+    pr = _problem(M, K, N, ydt, split_k, group, sparse, flags)
+    tcs = tc.struct()
+    _check(lib.fq_w4a16_outlier_matmul_noalloc(C.byref(pr), X.data_ptr(), Wq.data_ptr(),
+                                               scales.data_ptr(), zeros.data_ptr(),
+                                               C.byref(tcs), Y.data_ptr(),
+                                               _stream_handle(stream, X.device)),
+           "fq_w4a16_outlier_matmul_noalloc")
     return Y
 
 

@@ -5,6 +5,8 @@
 #include "fq.h"
 #include "internal.hpp"
 
+static_assert(FQ_NOALLOC_SCRATCH_BYTES == fqi::kScratchBytes, "static scratch size in fq.h");
+
 namespace {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
@@ -126,6 +128,7 @@ const char* fq_status_string(fq_status s) {
     case FQ_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case FQ_ERR_HIP: return "HIP runtime error at launch";
     case FQ_ERR_ALIGN: return "device pointer misaligned";
+    case FQ_ERR_SCRATCH_LIMIT: return "problem needs more scratch than the static maximum";
   }
   return "unknown status";
 }
@@ -194,6 +197,25 @@ fq_status fq_w4a16_outlier_matmul(const fq_problem* pr, const uint16_t* X, const
   if (st == FQ_OK) st = check_tc(pr, tc);
   if (st != FQ_OK) return st;
   return run(pr, X, Wq, scales, zeros, tc, Y, workspace, workspace_bytes, stream, true, true,
+             nullptr);
+}
+
+fq_status fq_w4a16_outlier_matmul_noalloc(const fq_problem* pr, const uint16_t* X,
+                                          const uint32_t* Wq, const uint16_t* scales,
+                                          const uint32_t* zeros, const fq_tilecoo_dev* tc,
+                                          void* Y, void* stream) {
+  fq_status st = check_problem(pr);
+  if (st == FQ_OK) st = check_dense_ptrs(X, Wq, scales, zeros, Y);
+  if (st == FQ_OK) st = check_tc(pr, tc);
+  if (st != FQ_OK) return st;
+  // the same plan the workspace entry point makes; its workspace must fit
+  // the static scratch (checked before the device is touched)
+  fqi::Plan plan;
+  if (!plan_for(pr, tc, true, true, &plan)) return FQ_ERR_UNSUPPORTED;
+  if (plan.ws_bytes > fqi::kScratchBytes) return FQ_ERR_SCRATCH_LIMIT;
+  void* scratch = nullptr;
+  if (fqi::scratch_for_current_device(&scratch, stream) != 0) return FQ_ERR_HIP;
+  return run(pr, X, Wq, scales, zeros, tc, Y, scratch, fqi::kScratchBytes, stream, true, true,
              nullptr);
 }
 

@@ -21,6 +21,11 @@ constexpr int kImageBytes = 16384;   // one wave's B-operand image of a 128 x 64
 // different shapes never finds partial sums where a counter is expected.
 constexpr size_t kCounterRegion = 256 * 1024;
 constexpr int kMaxStrips = int(kCounterRegion / 4);
+// Static device scratch of the allocation-free entry point: the counter
+// region followed by room for the split-K partial sums (8 MiB: every launch
+// plan of the Llama-3-8B/-70B decode and larger-M workloads needs at most
+// 4 MiB of them).
+constexpr size_t kScratchBytes = kCounterRegion + (size_t(8) << 20);
 
 // Launch plan of one matmul kernel.  Everything that sizes the workspace
 // depends only on (M, K, N, split_k) so the workspace can be sized before the
@@ -79,6 +84,12 @@ struct MatmulPtrs {
 
 // Enqueues one matmul kernel; returns a hipError_t value (0 on success).
 int launch_matmul(const Plan& plan, const MatmulPtrs& p, bool dense, bool sparse, void* stream);
+
+// The calling thread's current device's copy of the static scratch array
+// (kScratchBytes, 256-byte aligned).  Set up once per device: the array's
+// device address is looked up and its counter region cleared by a kernel on
+// `stream`.  Returns a hipError_t value (0 on success).
+int scratch_for_current_device(void** ptr, void* stream);
 
 // Enqueues the group decoder over every group; returns a hipError_t value.
 int launch_decode(const uint32_t* tile_indptr, int64_t n_tiles, const uint32_t* packed,

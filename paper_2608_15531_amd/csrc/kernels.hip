@@ -51,7 +51,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstddef>
+#include <mutex>
 #include <type_traits>
 
 #include "device.hpp"
@@ -1243,9 +1245,55 @@ int launch_mode(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool spars
   return launch_strip<MB, MODE, 4>(pl, a, dense, sparse, s);
 }
 
+// Scratch of the allocation-free entry point: the workspace of a matmul
+// call (arrival counters, then split-K partial sums) for callers that cannot
+// allocate device memory.  One copy per device, held until the process
+// ends.  Host code never passes this name to a kernel: it is a host-side
+// stand-in; the device address comes from hipGetSymbolAddress.
+__device__ __align__(256) unsigned char scratch[fqi::kScratchBytes];
+
+__global__ void __launch_bounds__(256) clear_words(uint32_t* p, uint32_t n) {
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
 }  // namespace fqk
 
 namespace fqi {
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+}  // namespace
+
+int scratch_for_current_device(void** ptr, void* stream) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return int(e);
+  if (dev < 0 || dev >= kMaxDevices) return int(hipErrorInvalidDevice);
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(fqk::scratch));
+      if (e != hipSuccess) return int(e);
+      if (!p) return int(hipErrorInvalidSymbol);
+      // the arrival counters must start at zero (every completed call
+      // leaves them at zero again): clear them once, in stream order
+      // before this first call's kernel
+      constexpr uint32_t n = uint32_t(kCounterRegion / 4);
+      hipLaunchKernelGGL(fqk::clear_words, dim3((n + 255) / 256), dim3(256), 0,
+                         static_cast<hipStream_t>(stream), static_cast<uint32_t*>(p), n);
+      e = hipGetLastError();
+      if (e != hipSuccess) return int(e);
+      g_scratch[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return 0;
+}
 
 namespace {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

@@ -69,7 +69,7 @@ def test_default_params(lib):
 
 
 def test_status_strings(lib):
-    for s in range(11):
+    for s in range(12):
         assert fq.fq_status_string(s) and fq.fq_status_string(s) != "unknown status"
     assert fq.fq_status_string(0) == "ok"
 
@@ -323,6 +323,37 @@ def test_matmul_rejects_bad_pointers(lib):
     assert _call(lib, pr, Y=FAKE + 8) == "FQ_ERR_ALIGN"
     assert lib.fq_w4a16_outlier_matmul(C.byref(pr), FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
                                        1 << 30, None) == 1
+
+
+def _call_noalloc(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE):
+    tc = tc if tc is not None else _tc()
+    return fq.STATUS_NAMES[lib.fq_w4a16_outlier_matmul_noalloc(C.byref(pr), X, Wq, s, z,
+                                                               C.byref(tc), Y, None)]
+
+
+def test_noalloc_rejects_before_touching_the_device(lib):
+    """The allocation-free entry point checks its arguments like the fused one
+    and rejects a problem whose launch plan needs more workspace than its
+    static scratch, all before any device call (this container has no GPU)."""
+    assert fq.NOALLOC_SCRATCH_BYTES == 256 * 1024 + (8 << 20)
+    with open(os.path.join(ROOT, "include", "fq.h")) as f:
+        assert "#define FQ_NOALLOC_SCRATCH_BYTES ((size_t)(256 * 1024 + (8 << 20)))" in f.read()
+    assert _call_noalloc(lib, _problem(M=0)) == "FQ_ERR_SHAPE"
+    assert _call_noalloc(lib, _problem(), X=None) == "FQ_ERR_NULL"
+    assert _call_noalloc(lib, _problem(), Y=FAKE + 8) == "FQ_ERR_ALIGN"
+    assert _call_noalloc(lib, _problem(), tc=_tc(params={"k_tile": 64})) == "FQ_ERR_UNSUPPORTED"
+    # explicit split-K over many strips: 448 strips x 8 splits x 32 rows x 64 x 4 B of partials
+    big = _problem(M=16, K=4096, N=28672, split_k=8)
+    need = C.c_size_t(0)
+    assert lib.fq_workspace_bytes(C.byref(big), C.byref(need)) == 0
+    assert need.value > fq.NOALLOC_SCRATCH_BYTES
+    assert _call_noalloc(lib, big) == "FQ_ERR_SCRATCH_LIMIT"
+    # every decode workload's default plan fits the static scratch
+    for M, K, N in [(16, 14336, 4096), (16, 28672, 8192), (32, 28672, 8192), (1, 4096, 6144),
+                    (128, 14336, 4096), (128, 4096, 14336), (16, 8192, 57344)]:
+        pr = _problem(M=M, K=K, N=N)
+        assert lib.fq_workspace_bytes(C.byref(pr), C.byref(need)) == 0
+        assert need.value <= fq.NOALLOC_SCRATCH_BYTES, (M, K, N, need.value)
 
 
 def test_matmul_rejects_bad_tilecoo(lib):
