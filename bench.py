@@ -819,6 +819,120 @@ def sweep(fq, torch, which, dev, copies_min=4):
             print(json.dumps(rec), flush=True)
 
 
+# Tile-COO packings compared for the element-reordering study (Sec. 3.2.2):
+# (name, params) over the same outliers
+PACKINGS = [
+    ("bucket1_none", {"group_mode": 1, "buckets_per_tile": 1, "reorder": 0}),
+    ("bucket1_columns", {"group_mode": 1, "buckets_per_tile": 1, "reorder": 1}),
+    ("bucket1_re_k2_4", {"group_mode": 1, "buckets_per_tile": 1, "reorder": 3,
+                         "elems_per_bank": 2, "n_bank_groups": 4}),
+    ("bucket1_re_k1_4", {"group_mode": 1, "buckets_per_tile": 1, "reorder": 3,
+                         "elems_per_bank": 1, "n_bank_groups": 4}),
+    ("bucket1_re_k1_8", {"group_mode": 1, "buckets_per_tile": 1, "reorder": 3,
+                         "elems_per_bank": 1, "n_bank_groups": 8}),
+    ("bucket16_re_k2_4", {"group_mode": 1, "buckets_per_tile": 16, "reorder": 3,
+                          "elems_per_bank": 2, "n_bank_groups": 4}),
+    ("column16_none", {"group_mode": 0, "buckets_per_tile": 16, "reorder": 0}),
+    ("column16_re_k2_4", {"group_mode": 0, "buckets_per_tile": 16, "reorder": 3,
+                          "elems_per_bank": 2, "n_bank_groups": 4}),
+]
+PACKING_CASES = [("gate_up", 4096, 28672, 1), ("gate_up", 4096, 28672, 16), ("o", 4096, 4096, 1)]
+
+
+def packing_pass(fq, torch, dev, timing: bool, R: int = 8):
+    """The fused kernel on each Tile-COO packing of PACKINGS over the same
+    outliers (PACKING_CASES).  timing: graph-replayed us per launch (JSON line
+    per case); else eager launches, one per rotated copy, for a rocprofv3
+    --pmc pass of the LDS counters (one JSON line names the sequence)."""
+    from synth import make_activations, make_problem, seed_for
+    si_of = {n: i for i, (n, _, _) in enumerate(SHAPES)}
+    seq, rows = [], []
+    for name, K, N, M in PACKING_CASES:
+        p = make_problem(1, K, N, frac=FRAC, seed=seed_for(1, si_of[name], 0))
+        W = [fq.to_device(p, dev)[1:] for _ in range(R)]
+        x = torch.from_numpy(make_activations(M, K, seed_for(1, si_of[name], MS.index(M)))
+                             .view(np.int16).copy()).view(torch.bfloat16).to(dev)
+        Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        ws = torch.zeros(fq.fq_workspace_bytes(M, K, N), dtype=torch.uint8, device=dev)
+        row = {"case": f"{name}/M{M}"}
+        for pname, prm in PACKINGS:
+            host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v, prm)
+            T = [fq.TileCOODevice(host, dev) for _ in range(R)]
+            fn = lambda i: fq.fq_w4a16_outlier_matmul(x, *W[i % R], T[i % R], Y=Y, ws=ws)
+            if timing:
+                g = capture_graph(torch, lambda: [fn(i) for i in range(4 * R)])
+                row[pname] = round(graph_us(torch, g, 4 * R, max(2, 160 // (4 * R))), 3)
+                row[pname + "_groups"] = int(host.sizes.n_groups)
+                del g
+            else:
+                for i in range(R):
+                    fn(i)
+                torch.cuda.synchronize()
+                seq.append({"case": row["case"], "packing": pname, "launches": R,
+                            "groups": int(host.sizes.n_groups)})
+            del T
+        if timing:
+            print(json.dumps(row), flush=True)
+            rows.append(row)
+        del W
+        torch.cuda.empty_cache()
+    if not timing:
+        print(json.dumps({"packing_pass": seq}), flush=True)
+
+
+def packing_summary(csv_path, pass_log, timing_log):
+    """Markdown on stdout: LDS bank-conflict counters and times of the fused
+    kernel per Tile-COO packing (--packing-pass under rocprofv3 --pmc, and
+    --packing-sweep).  No GPU."""
+    import csv
+    seq = _json_lines(pass_log, '{"packing_pass"')[0]["packing_pass"]
+    times = {r["case"]: r for r in _json_lines(timing_log, '{"case"')}
+    disp = {}
+    for r in csv.DictReader(open(csv_path)):
+        if "matmul_kernel" not in r["Kernel_Name"]:
+            continue
+        d = disp.setdefault(int(r["Dispatch_Id"]), {})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    ds = [disp[k] for k in sorted(disp)]
+    need = sum(c["launches"] for c in seq)
+    if len(ds) < need:
+        raise SystemExit(f"{len(ds)} fused dispatches, expected {need}")
+    ds = ds[len(ds) - need:]   # the warm-up launches of bench's main() come first
+    out = ["# LDS bank conflicts of the outlier scatter against the Tile-COO packing "
+           "(element reordering, Sec. 3.2.2)", "",
+           "Commands (repo root, MI355X, ROCm 7.2; `export TMPDIR=/tmp` first), then this "
+           "summary (no GPU):", "",
+           "    timeout -s KILL 200 rocprofv3 --pmc SQ_LDS_BANK_CONFLICT SQ_ACTIVE_INST_LDS "
+           "SQ_INSTS_LDS GRBM_GUI_ACTIVE --output-format csv -d gpurun_out/pmc_pack -o run -- "
+           "python3 -u bench.py --packing-pass > gpurun_out/pmc_pack.log",
+           "    python3 -u bench.py --packing-sweep > gpurun_out/packing_sweep.log",
+           "    python bench.py --packing-summary gpurun_out/pmc_pack/run_counter_collection.csv "
+           "gpurun_out/pmc_pack.log gpurun_out/packing_sweep.log "
+           "> profiles/lds_bank_conflicts_packing.md", "",
+           "The same 1 % uniform outliers packed eight ways; the fused kernel in its default "
+           "launch plan (the MFMA outlier mapping: each lane writes the four values of one "
+           "16-byte group into an LDS image of the tile's B operand, 2-byte stores, so the 64 "
+           "lanes of one store hold the same slot of 64 different groups).  Counters per "
+           "launch (mean of 8, one per rotated weight copy); time per launch from graph "
+           "replays.  `re_kE_G`: element reordering with bank group (k / E) % G, rotated per "
+           "bucket.", "",
+           "| case | packing | groups | LDS instructions | LDS-active cycles | bank-conflict "
+           "cycles | conflict / active | us per launch |",
+           "|---|---|---|---|---|---|---|---|"]
+    i = 0
+    for c in seq:
+        d = ds[i:i + c["launches"]]
+        i += c["launches"]
+        n = len(d)
+        ins = sum(x.get("SQ_INSTS_LDS", 0) for x in d) / n
+        act = sum(x.get("SQ_ACTIVE_INST_LDS", 0) for x in d) / n
+        con = sum(x.get("SQ_LDS_BANK_CONFLICT", 0) for x in d) / n
+        us = times.get(c["case"], {}).get(c["packing"])
+        out.append(f"| {c['case']} | {c['packing']} | {c['groups']} | {ins:.4g} | {act:.4g} | "
+                   f"{con:.4g} | {con / max(act, 1):.3f} | {us if us is not None else '-'} |")
+    print("\n".join(out))
+
+
 TRACE_WARM, TRACE_REPS = 2, 6   # replays per case in the kernel-trace pass
 
 
@@ -992,6 +1106,14 @@ def main():
     ap.add_argument("--trace-per-matmul", nargs=2, metavar=("KERNEL_TRACE_CSV", "LOG"),
                     help="no GPU: per-matmul kernel-only durations from a --trace-pass run's "
                          "kernel trace")
+    ap.add_argument("--packing-pass", action="store_true",
+                    help="eager fused launches per Tile-COO packing (element reordering "
+                         "study) for a rocprofv3 --pmc pass of the LDS counters")
+    ap.add_argument("--packing-sweep", action="store_true",
+                    help="graph-replayed us per launch of the fused kernel per Tile-COO packing")
+    ap.add_argument("--packing-summary", nargs=3, metavar=("CSV", "PASS_LOG", "SWEEP_LOG"),
+                    help="no GPU: the LDS bank-conflict profile from --packing-pass and "
+                         "--packing-sweep")
     ap.add_argument("--sweep-summary", nargs=5,
                     metavar=("DENSITY_LOG", "70B_LOG", "LARGE_M_LOG", "MFMA_CSV", "MFMA_LOG"),
                     help="no GPU: the sweeps profile text from the three --sweep outputs and "
@@ -999,6 +1121,9 @@ def main():
     args = ap.parse_args()
     if args.trace_per_matmul:
         trace_per_matmul(*args.trace_per_matmul)
+        return
+    if args.packing_summary:
+        packing_summary(*args.packing_summary)
         return
     if args.trace_summary:
         trace_summary(*args.trace_summary)
@@ -1036,6 +1161,9 @@ def main():
         return
     if args.pmc_pass_large_m:
         pmc_pass_large_m(fq, torch, dev)
+        return
+    if args.packing_pass or args.packing_sweep:
+        packing_pass(fq, torch, dev, timing=args.packing_sweep)
         return
 
     # ---------------------------------------------------------- inputs
