@@ -50,19 +50,21 @@ PROBE_CONFIGS = [(256, 8, 4), (512, 4, 4), (512, 8, 2), (1024, 4, 2), (1024, 4, 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fused_llama3_8b_decode_traffic.md")
 
 
-def kernel_name(fq, M, K, N, packing=None):
-    """Template instance of the fused kernel the library launches for (M, K, N)
-    and a Tile-COO packed with `packing` (default: the library default)."""
+def kernel_name(fq, M, K, N, packing=None, flags=0):
+    """Template instance of the fused kernel the library launches for (M, K, N),
+    a Tile-COO packed with `packing` (default: the library default) and the
+    switches `flags`."""
     packing = packing or {}
     c = fq.fq_launch_config(M, K, N, buckets_per_tile=packing.get("buckets_per_tile"),
-                            group_mode=packing.get("group_mode"))
+                            group_mode=packing.get("group_mode"), flags=flags)
     mb = 1 if min(M, 32) <= 16 else 2
     mode = 0 if c["mapping"] == "gather" else 1
     sk = "true" if c["stream_k"] else "false"
     xs = c["x_stage_loads"]
     bk = "true" if c["bulk_scales"] else "false"
+    dv = "true" if flags & fq.FQ_DENSE_VALU else "false"
     return (f"matmul_kernel<{mb}, {mode}, {c['strip_cols'] // 16}, true, true, "
-            f"{c['dense_waves']}, {sk}, {c['outlier_waves']}, {xs}, {bk}>")
+            f"{c['dense_waves']}, {sk}, {c['outlier_waves']}, {xs}, {bk}, {dv}>")
 
 
 def dominant_kernel(fq, cases):
@@ -215,6 +217,11 @@ def pmc_summary(fetch_csv, write_csv, sq_csv, log_path):
     if meta is None:
         raise SystemExit(f"no pmc_pass line in {log_path}")
     kernel = meta["kernel"]
+    narrow = meta.get("role") == "narrow"
+    flag = "--pmc-pass-narrow" if narrow else "--pmc-pass"
+    sfx = "_narrow" if narrow else ""
+    dest = ("profiles/fused_llama3_8b_decode_narrow_traffic.md" if narrow
+            else "profiles/fused_llama3_8b_decode_traffic.md")
 
     def read(path):
         rows = {}
@@ -242,22 +249,24 @@ def pmc_summary(fetch_csv, write_csv, sq_csv, log_path):
     write = sum(wd) / len(wd) * 1024 * wf
     alg = meta["algorithmic_bytes_per_launch"]
     cases = meta["pmc_pass"]
-    out = ["# Fused W4A16 outlier matmul, dominant kernel: HBM traffic and SQ counters", "",
+    title = ("narrow-strip kernel (qkv and o)" if narrow else "dominant kernel")
+    out = [f"# Fused W4A16 outlier matmul, {title}: HBM traffic and SQ counters", "",
            "Commands (repo root, MI355X, ROCm 7.2; `export TMPDIR=/tmp` first), one counter "
            "pass each, then this summary (no GPU):", "",
            "    timeout -s KILL 150 rocprofv3 --pmc FETCH_SIZE --output-format csv -d "
-           "gpurun_out/pmc_fetch -o run -- python3 -u bench.py --pmc-pass "
-           "> gpurun_out/pmc_fetch.log",
+           f"gpurun_out/pmc_fetch{sfx} -o run -- python3 -u bench.py {flag} "
+           f"> gpurun_out/pmc_fetch{sfx}.log",
            "    timeout -s KILL 150 rocprofv3 --pmc WRITE_SIZE --output-format csv -d "
-           "gpurun_out/pmc_write -o run -- python3 -u bench.py --pmc-pass",
+           f"gpurun_out/pmc_write{sfx} -o run -- python3 -u bench.py {flag}",
            "    timeout -s KILL 150 rocprofv3 --pmc SQ_WAVE_CYCLES SQ_BUSY_CYCLES "
            "SQ_ACTIVE_INST_VALU SQ_VALU_MFMA_BUSY_CYCLES SQ_LDS_BANK_CONFLICT SQ_ACTIVE_INST_LDS "
-           "SQ_INSTS_VALU SQ_WAVES GRBM_GUI_ACTIVE --output-format csv -d gpurun_out/pmc_sq "
-           "-o run -- python3 -u bench.py --pmc-pass",
-           "    python bench.py --pmc-summary gpurun_out/pmc_fetch/run_counter_collection.csv "
-           "gpurun_out/pmc_write/run_counter_collection.csv "
-           "gpurun_out/pmc_sq/run_counter_collection.csv gpurun_out/pmc_fetch.log "
-           "> profiles/fused_llama3_8b_decode_traffic.md", "",
+           f"SQ_INSTS_VALU SQ_WAVES GRBM_GUI_ACTIVE --output-format csv -d gpurun_out/pmc_sq{sfx} "
+           f"-o run -- python3 -u bench.py {flag}",
+           "    python bench.py --pmc-summary "
+           f"gpurun_out/pmc_fetch{sfx}/run_counter_collection.csv "
+           f"gpurun_out/pmc_write{sfx}/run_counter_collection.csv "
+           f"gpurun_out/pmc_sq{sfx}/run_counter_collection.csv gpurun_out/pmc_fetch{sfx}.log "
+           f"> {dest}", "",
            "(the .log file is the stdout of the first pass, which names the launches)", "",
            f"Kernel `{kernel}`: launches {', '.join(cases)} of the Llama-3-8B decode step, "
            f"each once per rotated weight copy ({meta['copies']} copies), then one plain device "
@@ -302,10 +311,14 @@ def pmc_summary(fetch_csv, write_csv, sq_csv, log_path):
            "hbm_bytes_per_launch": round(fetch + write), "fetch_bytes_per_launch": round(fetch),
            "write_bytes_per_launch": round(write), "algorithmic_bytes_per_launch": round(alg),
            "fetch_factor": round(ff, 5), "write_factor": round(wf, 5), "launches": len(fd)}
-    out += ["", "bench.py reads the line below and reports `hbm_bytes_per_launch` as "
-                "roofline.traffic only while the kernel sources still hash to "
-                "`kernel_sources_sha256` and the dominant kernel is the same instance.", "",
-            "traffic_json: " + json.dumps(rec)]
+    if narrow:
+        out += ["", "The same figures as a record (bench.py takes roofline.traffic from the "
+                    "dominant kernel's summary only).", "", "traffic_json: " + json.dumps(rec)]
+    else:
+        out += ["", "bench.py reads the line below and reports `hbm_bytes_per_launch` as "
+                    "roofline.traffic only while the kernel sources still hash to "
+                    "`kernel_sources_sha256` and the dominant kernel is the same instance.", "",
+                "traffic_json: " + json.dumps(rec)]
     print("\n".join(out))
 
 
@@ -583,11 +596,13 @@ def trace_summary(stats_csv, traced_log, plain_log):
            "(by-bucket groups, one bucket per tile; the paper-format step of the same run, "
            "by-column groups with 16 buckets, is included in the counts); 8 rotated weight "
            "copies per shape (graph replay).", "",
-           "`matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR>`: MB 16-row blocks; "
-           "MODE 0 = LDS-gather outlier mapping, 1 = MFMA image mapping; NCB 16-column MFMA "
-           "blocks per strip (2: 32-column strips, 4: 64-column strips); NW waves per workgroup; "
-           "SK Stream-K; NWS extra outlier-only waves; XR row-wise X loads per tile reordered "
-           "through LDS (ceil(M/4); 0 = loads in operand order).", "",
+           "`matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR, BK, DV>`: MB 16-row "
+           "blocks; MODE 0 = LDS-gather outlier mapping, 1 = MFMA image mapping; NCB 16-column "
+           "MFMA blocks per strip (2: 32-column strips, 4: 64-column strips); NW waves per "
+           "workgroup; SK Stream-K; NWS extra outlier-only waves; XR row-wise X loads per tile "
+           "reordered through LDS (ceil(M/4); 0 = loads in operand order); BK scales and "
+           "zero-points loaded once per wave; DV dense products by VALU dot products "
+           "(ablation).", "",
            f"Kernel sources sha256 (kernels.hip, device.hpp, internal.hpp): "
            f"`{kernel_source_digest()}`", "",
            "| kernel | launches (shapes, default packing) | calls | total ns | average ns | min ns "
@@ -933,6 +948,119 @@ def packing_summary(csv_path, pass_log, timing_log):
     print("\n".join(out))
 
 
+DENSE_PATH_COUNTERS = ("SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_ACTIVE_INST_VALU SQ_VALU_MFMA_BUSY_CYCLES "
+                       "SQ_INSTS_VALU SQ_WAVES GRBM_GUI_ACTIVE")
+
+
+def dense_path_pass(fq, torch, dev, timing: bool, R: int = 8):
+    """The dense path on MFMA (the default at every M) against the same kernel
+    with FQ_DENSE_VALU (VALU bf16 dot products, a GEMV), at one row on the
+    Llama-3-8B decode shapes: fused and dense-only.  timing: graph-replayed us
+    per launch (JSON line per shape); else eager launches, one per rotated
+    copy, for a rocprofv3 --pmc pass (one JSON line names the sequence)."""
+    from synth import make_activations, make_problem, seed_for
+    M = 1
+    seq = []
+    for si, (name, K, N) in enumerate(SHAPES):
+        p = make_problem(1, K, N, frac=FRAC, seed=seed_for(1, si, 0))
+        host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v)
+        W = [fq.to_device(p, dev)[1:] for _ in range(R)]
+        T = [fq.TileCOODevice(host, dev) for _ in range(R)]
+        x = torch.from_numpy(make_activations(M, K, seed_for(1, si, 0)).view(np.int16).copy())
+        x = x.view(torch.bfloat16).to(dev)
+        Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        ws = torch.zeros(fq.fq_workspace_bytes(M, K, N), dtype=torch.uint8, device=dev)
+        row = {"case": f"{name}/M{M}", "bytes": algorithmic_bytes(M, K, N, host.sizes.bytes)}
+        for variant, dense_only, flags in (("fused_mfma", False, 0),
+                                           ("fused_valu", False, fq.FQ_DENSE_VALU),
+                                           ("dense_mfma", True, 0),
+                                           ("dense_valu", True, fq.FQ_DENSE_VALU)):
+            if dense_only:
+                fn = lambda i, f=flags: fq.fq_w4a16_matmul(x, *W[i % R], Y=Y, ws=ws, flags=f)
+            else:
+                fn = lambda i, f=flags: fq.fq_w4a16_outlier_matmul(x, *W[i % R], T[i % R], Y=Y,
+                                                                    ws=ws, flags=f)
+            if timing:
+                g = capture_graph(torch, lambda: [fn(i) for i in range(4 * R)])
+                row[variant] = round(graph_us(torch, g, 4 * R, max(2, 160 // (4 * R))), 3)
+                del g
+            else:
+                for i in range(R):
+                    fn(i)
+                torch.cuda.synchronize()
+                seq.append({"case": row["case"], "variant": variant, "launches": R})
+        if timing:
+            row["kernel_mfma"] = kernel_name(fq, M, K, N)
+            row["kernel_valu"] = kernel_name(fq, M, K, N, flags=fq.FQ_DENSE_VALU)
+            print(json.dumps(row), flush=True)
+        del W, T
+        torch.cuda.empty_cache()
+    if not timing:
+        print(json.dumps({"dense_path_pass": seq}), flush=True)
+
+
+def dense_path_summary(csv_path, pass_log, timing_log):
+    """Markdown on stdout: time and SQ counters of the dense path on MFMA
+    against VALU dot products at one row (--dense-path-pass under rocprofv3
+    --pmc, and --dense-path-sweep).  No GPU."""
+    import csv
+    seq = _json_lines(pass_log, '{"dense_path_pass"')[0]["dense_path_pass"]
+    times = {r["case"]: r for r in _json_lines(timing_log, '{"case"')}
+    disp = {}
+    for r in csv.DictReader(open(csv_path)):
+        if "matmul_kernel" not in r["Kernel_Name"]:
+            continue
+        d = disp.setdefault(int(r["Dispatch_Id"]), {})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    ds = [disp[k] for k in sorted(disp)]
+    need = sum(c["launches"] for c in seq)
+    if len(ds) < need:
+        raise SystemExit(f"{len(ds)} matmul dispatches, expected {need}")
+    ds = ds[len(ds) - need:]   # the warm-up launches of bench's main() come first
+    out = ["# Dense path at one row: MFMA (the default) against VALU dot products (a GEMV)", "",
+           "Commands (repo root, MI355X, ROCm 7.2; `export TMPDIR=/tmp` first), then this "
+           "summary (no GPU):", "",
+           f"    timeout -s KILL 200 rocprofv3 --pmc {DENSE_PATH_COUNTERS} --output-format csv "
+           "-d gpurun_out/pmc_dense -o run -- python3 -u bench.py --dense-path-pass "
+           "> gpurun_out/pmc_dense.log",
+           "    python3 -u bench.py --dense-path-sweep > gpurun_out/dense_path_sweep.log",
+           "    python bench.py --dense-path-summary gpurun_out/pmc_dense/run_counter_collection.csv "
+           "gpurun_out/pmc_dense.log gpurun_out/dense_path_sweep.log "
+           "> profiles/dense_path_mfma_vs_valu_m1.md", "",
+           "The same kernel, loads, tiles and outlier path; only the dense products differ.  "
+           "`mfma`: each lane's dequantised codes are the B operand of "
+           "v_mfma_f32_16x16x32_bf16 (one MFMA per 16 columns and 32 k, plus one per 32 k for "
+           "the row sums that remove the zero-points).  `valu` (FQ_DENSE_VALU): the same codes "
+           "multiplied with the lane's X values by v_dot2_f32_bf16 (four per packed word), "
+           "the lane's k-chunk sums added across lanes after the last tile.  One row (M = 1, "
+           "where a GEMV does the least extra work), 1 % outliers in the default packing, "
+           "rotated weight copies; time per launch from graph replays, counters per launch "
+           "(mean of the 8 launches, one per copy).  VALU-active is a fraction of the summed "
+           "wave cycles; MFMA-busy cycles are the counter's sum over the chip per launch "
+           "(compare across rows, not against a peak).", "",
+           "| case | variant | us per launch | GB/s | VALU instructions per wave | VALU-active / "
+           "wave cycles | MFMA-busy cycles per launch | waves |",
+           "|---|---|---|---|---|---|---|---|"]
+    i = 0
+    for c in seq:
+        d = ds[i:i + c["launches"]]
+        i += c["launches"]
+        n = len(d)
+        get = lambda k: sum(x.get(k, 0.0) for x in d) / n
+        waves = get("SQ_WAVES")
+        t = times.get(c["case"], {})
+        us = t.get(c["variant"])
+        gbs = f"{t['bytes'] / us / 1e3:.0f}" if us else "-"
+        out.append(f"| {c['case']} | {c['variant']} | {us if us is not None else '-'} | {gbs} | "
+                   f"{get('SQ_INSTS_VALU') / max(waves, 1):.0f} | "
+                   f"{get('SQ_ACTIVE_INST_VALU') / max(get('SQ_WAVE_CYCLES'), 1):.3f} | "
+                   f"{get('SQ_VALU_MFMA_BUSY_CYCLES'):.4g} | "
+                   f"{waves:.0f} |")
+    kern = {r["case"]: (r.get("kernel_mfma"), r.get("kernel_valu")) for r in times.values()}
+    out += ["", "Kernel instances: " + "; ".join(f"{k}: `{a}` / `{b}`" for k, (a, b) in kern.items())]
+    print("\n".join(out))
+
+
 TRACE_WARM, TRACE_REPS = 2, 6   # replays per case in the kernel-trace pass
 
 
@@ -1082,6 +1210,15 @@ def main():
                     help="no timing: eager launches of the dominant kernel's matmuls over the "
                          "rotated copies, then a plain copy of COPY_CAL_BYTES, for rocprofv3 "
                          "--pmc FETCH_SIZE / WRITE_SIZE collection")
+    ap.add_argument("--pmc-pass-narrow", action="store_true",
+                    help="as --pmc-pass, for the 32-column-strip instance of qkv and o at one row")
+    ap.add_argument("--dense-path-pass", action="store_true",
+                    help="eager launches of the dense path on MFMA and on VALU dot products "
+                         "(FQ_DENSE_VALU) at one row, for a rocprofv3 --pmc pass")
+    ap.add_argument("--dense-path-sweep", action="store_true",
+                    help="graph-replayed times of the same comparison")
+    ap.add_argument("--dense-path-summary", nargs=3, metavar=("CSV", "PASS_LOG", "SWEEP_LOG"),
+                    help="no GPU: summarise --dense-path-pass counters and --dense-path-sweep times")
     ap.add_argument("--sweep", choices=["density", "70b", "large-m"],
                     help="no step timing: per-matmul timings of the density / structure "
                          "sweep (M=8, 4096x14336), the Llama-3-70B decode linears (M=1..32) "
@@ -1125,6 +1262,9 @@ def main():
     if args.packing_summary:
         packing_summary(*args.packing_summary)
         return
+    if args.dense_path_summary:
+        dense_path_summary(*args.dense_path_summary)
+        return
     if args.trace_summary:
         trace_summary(*args.trace_summary)
         return
@@ -1161,6 +1301,9 @@ def main():
         return
     if args.pmc_pass_large_m:
         pmc_pass_large_m(fq, torch, dev)
+        return
+    if args.dense_path_pass or args.dense_path_sweep:
+        dense_path_pass(fq, torch, dev, timing=args.dense_path_sweep)
         return
     if args.packing_pass or args.packing_sweep:
         packing_pass(fq, torch, dev, timing=args.packing_sweep)
@@ -1220,10 +1363,16 @@ def main():
         ablation(fq, torch, cases, order, ws, R, dev, capture_fn=None)
         return
 
-    if args.pmc_pass:
-        # Each dominant-kernel matmul once per weight copy, then the copy
-        # kernel whose byte count calibrates the counters.
-        dom_name, dom = dominant_kernel(fq, order)
+    if args.pmc_pass or args.pmc_pass_narrow:
+        # Each matmul of the dominant instance (or of the narrow-strip instance
+        # of qkv and o at one row) once per weight copy, then the copy kernel
+        # whose byte count calibrates the counters.
+        if args.pmc_pass_narrow:
+            qkv = next(c for c in order if c.name == "qkv" and c.M == 1)
+            dom_name = kernel_name(fq, 1, qkv.K, qkv.N)
+            dom = [c for c in order if kernel_name(fq, c.M, c.K, c.N) == dom_name]
+        else:
+            dom_name, dom = dominant_kernel(fq, order)
         for r in range(R):
             for c in dom:
                 launch(c, r, "fused")
@@ -1233,6 +1382,7 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"pmc_pass": [f"{c.name}/M{c.M}" for c in dom], "kernel": dom_name,
+                          "role": "narrow" if args.pmc_pass_narrow else "dominant",
                           "copies": R,
                           "algorithmic_bytes_per_launch": sum(c.bytes for c in dom) / len(dom),
                           "copy_bytes": COPY_CAL_BYTES}), flush=True)

@@ -236,7 +236,8 @@ typedef struct {
  *   flags       bit set: one FQ_SPARSE_* value in bits 0-1 to force the
  *               sparse-path mapping (the library otherwise picks by M), and
  *               the schedule switches FQ_SCHED_STREAM_K, FQ_FOUR_WAVES,
- *               FQ_STRIP_32, FQ_STRIP_64 and FQ_SPARSE_WAVES.
+ *               FQ_STRIP_32, FQ_STRIP_64 and FQ_SPARSE_WAVES, and the dense-path
+ *               switch FQ_DENSE_VALU.
  */
 typedef struct {
   int32_t M;
@@ -284,6 +285,15 @@ enum { FQ_STRIP_32 = 16, FQ_STRIP_64 = 32 };
  * much as the dense path when run alone, and interleaving the two in one
  * wave hides their latencies better than splitting them. */
 enum { FQ_SPARSE_WAVES = 64 };
+
+/* Dense-path products on the vector ALUs (fq_problem.flags), for ablation.
+ * By default X . dequant(W_Q) runs on MFMA at every M.  FQ_DENSE_VALU instead
+ * multiplies each lane's dequantised codes with its X values by bf16 dot
+ * products (v_dot2_f32_bf16), a GEMV on the vector ALUs; same loads, tiles
+ * and outlier path.  M == 1 only, not with FQ_SPARSE_GATHER,
+ * FQ_SCHED_STREAM_K or FQ_SPARSE_WAVES (FQ_ERR_UNSUPPORTED otherwise); it
+ * applies to the fused, unfused and dense-only entry points. */
+enum { FQ_DENSE_VALU = 128 };
 
 /*
  * fq_workspace_bytes -- device workspace the matmul entry points need for

@@ -41,6 +41,7 @@ FQ_FOUR_WAVES = 8
 FQ_STRIP_32 = 16
 FQ_STRIP_64 = 32
 FQ_SPARSE_WAVES = 64
+FQ_DENSE_VALU = 128
 
 
 class FqError(RuntimeError):

@@ -19,7 +19,11 @@ fq_status check_problem(const fq_problem* pr) {
   if (pr->M > fqi::kMaxM) return FQ_ERR_UNSUPPORTED;
   if (pr->y_dtype != FQ_Y_BF16 && pr->y_dtype != FQ_Y_F32) return FQ_ERR_UNSUPPORTED;
   if (pr->flags & ~(FQ_SPARSE_MASK | FQ_SCHED_STREAM_K | FQ_FOUR_WAVES | FQ_STRIP_32 | FQ_STRIP_64 |
-                    FQ_SPARSE_WAVES))
+                    FQ_SPARSE_WAVES | FQ_DENSE_VALU))
+    return FQ_ERR_UNSUPPORTED;
+  if ((pr->flags & FQ_DENSE_VALU) &&
+      (pr->M != 1 || (pr->flags & (FQ_SCHED_STREAM_K | FQ_SPARSE_WAVES)) ||
+       (pr->flags & FQ_SPARSE_MASK) == FQ_SPARSE_GATHER))
     return FQ_ERR_UNSUPPORTED;
   const int mapping = pr->flags & FQ_SPARSE_MASK;
   if ((pr->flags & FQ_STRIP_32) &&
@@ -63,7 +67,8 @@ int plan_opts(const fq_problem* pr);
 int plan_mode(const fq_problem* pr, int32_t group_mode) {
   const int mapping = pr->flags & FQ_SPARSE_MASK;
   if (mapping == FQ_SPARSE_GATHER) return 0;
-  if (mapping == FQ_SPARSE_MFMA || group_mode == FQ_GROUP_BY_BUCKET) return 1;
+  if (mapping == FQ_SPARSE_MFMA || group_mode == FQ_GROUP_BY_BUCKET || (pr->flags & FQ_DENSE_VALU))
+    return 1;
   return -1;
 }
 
@@ -108,7 +113,8 @@ int plan_opts(const fq_problem* pr) {
          ((pr->flags & FQ_FOUR_WAVES) ? fqi::kOptFourWaves : 0) |
          ((pr->flags & FQ_STRIP_32) ? fqi::kOptStrip32 : 0) |
          ((pr->flags & FQ_STRIP_64) ? fqi::kOptStrip64 : 0) |
-         ((pr->flags & FQ_SPARSE_WAVES) ? fqi::kOptSparseWaves : 0);
+         ((pr->flags & FQ_SPARSE_WAVES) ? fqi::kOptSparseWaves : 0) |
+         ((pr->flags & FQ_DENSE_VALU) ? fqi::kOptDenseValu : 0);
 }
 
 }  // namespace

@@ -48,6 +48,7 @@ struct Plan {
   int B;             // buckets per tile
   int XS;            // row-wise X loads per tile through the LDS stage: 0, or 1, 2, 4 (ceil(M/4))
   int BK;            // 1: a dense wave loads the scales and zero-points of all its tiles at once
+  int DV;            // 1: dense products by VALU dot products instead of MFMA (one row; ablation)
   // dynamic LDS layout, bytes: one slot per wave (X slice or B-operand
   // image), then the gather-mode sparse output buffers or the X stages
   size_t slot_bytes, off_shc, off_flag, off_trash, off_xs, lds_bytes;
@@ -61,6 +62,7 @@ constexpr int kOptFourWaves = 2;   // never eight waves per workgroup
 constexpr int kOptStrip32 = 4;     // 32-column strips (MFMA outlier mapping, no Stream-K)
 constexpr int kOptStrip64 = 8;     // 64-column strips
 constexpr int kOptSparseWaves = 16;   // warp specialisation: outlier waves beside the dense waves
+constexpr int kOptDenseValu = 32;     // dense products by VALU dot products (M == 1, MFMA mapping)
 
 // Returns false when (M, K, N) is outside what the kernels implement.
 // mode: -1 picks the sparse mapping by M, 0 forces gathers, 1 forces MFMA.

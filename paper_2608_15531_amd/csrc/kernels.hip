@@ -535,7 +535,8 @@ __device__ __forceinline__ void clear_group(const uint32_t addr[4]) {
 // Two 16-row blocks hold the most registers; they are kept to two waves per
 // SIMD (half the register file), which every instance launched fits without
 // spilling.
-template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS, int XR, bool BK>
+template <int MB, int MODE, int NCB, bool KD, bool KS, int NW, bool SK, int NWS, int XR, bool BK,
+          bool DV>
 __global__ void __launch_bounds__(64 * (NW + NWS))
     __attribute__((amdgpu_waves_per_eu(MB == 2 ? 2 : 1))) matmul_kernel(
         const uint32_t* Wq, const uint16_t* scales, const uint32_t* zeros, const uint16_t* X,
@@ -550,6 +551,12 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
   constexpr bool WS = NWS > 0;
   static_assert(!WS || (KD && KS && MODE == 1 && !SK), "outlier waves: fused MFMA mapping, split-K");
   static_assert(!BK || (KD && !SK), "bulk scale loads: dense waves, uniform split-K");
+  // DV: the dense products on the vector ALUs (v_dot2_f32_bf16 of each lane's
+  // dequantised codes and its X values) instead of MFMA -- one row, the MFMA
+  // outlier mapping, one staged X load, every wave both paths.  An ablation
+  // of the default, which runs the dense path on MFMA at every M.
+  static_assert(!DV || (KD && MB == 1 && MODE == 1 && XR == 1 && NWS == 0 && !SK),
+                "dense dot products: one row, MFMA outlier mapping");
   constexpr int NC = 16 * NCB;                 // strip width, columns
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
@@ -692,6 +699,9 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
   int64_t tile_base = 0;
   uint32_t tp = 0;
   f32x4_t acc[MB][NCB];
+  // DV: the scaled dot products of this lane's k-chunk (rows 8h..8h+7 of
+  // each 32-row step), summed over the four chunks after the last tile
+  float accv[NCB];
   BulkRegs<NCB> bulk;   // BK: scales and zero-points of the wave's tiles
 
   // The tile pipeline of one wave for one role: dense and outlier work
@@ -772,12 +782,15 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       // groups, whose loads depend on tile_indptr and are issued last.
       constexpr bool SPM = SPARSE && MODE == 1;
       f32x4_t tmp[MB][NCB], xsum[MB];
+      float dv[NCB];
   #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         xsum[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   #pragma unroll
         for (int c = 0; c < NCB; ++c) tmp[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       }
+  #pragma unroll
+      for (int c = 0; c < NCB; ++c) dv[c] = 0.f;
       if (DENSE) {
   #pragma unroll
         for (int step = 0; step < 4; ++step) {
@@ -792,10 +805,20 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
             bf16x8_t Bq[2];
             dequant_pair(w4[c], w4[c + 1], Bq[0], Bq[1]);
   #pragma unroll
-            for (int e = 0; e < 2; ++e)
+            for (int e = 0; e < 2; ++e) {
+              if constexpr (DV) {
+                // the lane's 8 codes of column c+e against the 8 X values of
+                // the same k (A holds row 0 in the same pair order)
+                const u32x4_t b = __builtin_bit_cast(u32x4_t, Bq[e]);
+                const u32x4_t x = __builtin_bit_cast(u32x4_t, A[0][step]);
   #pragma unroll
-              for (int mb = 0; mb < MB; ++mb)
-                tmp[mb][c + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bq[e], tmp[mb][c + e], 0, 0, 0);
+                for (int j = 0; j < 4; ++j) dv[c + e] = dot2_bf16(b[j], x[j], dv[c + e]);
+              } else {
+  #pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+                  tmp[mb][c + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bq[e], tmp[mb][c + e], 0, 0, 0);
+              }
+            }
           }
   #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
@@ -823,15 +846,26 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
         const int zsh = ((NCB * c4) & 7) * 4;
   #pragma unroll
         for (int c = 0; c < NCB; ++c) zf[c] = kCodeOffset + float((cz >> (zsh + 4 * c)) & 15u);
+        if constexpr (DV) {
+          // every lane scales its chunk's sums; the zero-point term uses the
+          // tile's whole row sum (lanes h = 0 hold row 0 of the MFMA result)
+          const float xs0 = h == 0 ? xsum[0][0] : 0.f;
   #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-  #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            if (MB == 1 && r > 0 && r >= a.M) break;
-  #pragma unroll
-            for (int c = 0; c < NCB; ++c)
-              acc[mb][c][r] += sc[c] * (tmp[mb][c][r] - zf[c] * xsum[mb][r]);
+          for (int c = 0; c < NCB; ++c) {
+            accv[c] += sc[c] * dv[c];
+            acc[0][c][0] -= sc[c] * (zf[c] * xs0);
           }
+        } else {
+  #pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+  #pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              if (MB == 1 && r > 0 && r >= a.M) break;
+  #pragma unroll
+              for (int c = 0; c < NCB; ++c)
+                acc[mb][c][r] += sc[c] * (tmp[mb][c][r] - zf[c] * xsum[mb][r]);
+            }
+        }
       }
 
       // ---- sparse path, MFMA mapping: scatter the tile's outliers into the
@@ -1021,12 +1055,25 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int c = 0; c < NCB; ++c) acc[mb][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NCB; ++c) accv[c] = 0.f;
 
     if constexpr (WS) {
       if (swave) tiles(std::false_type{}, std::true_type{});
       else tiles(std::true_type{}, std::false_type{});
     } else {
       tiles(std::integral_constant<bool, KD>{}, std::integral_constant<bool, KS>{});
+    }
+    if constexpr (DV) {
+      // lanes (h, c4), h = 0..3, hold the four k-chunks of the same columns:
+      // sum them (fixed order) into row 0 of the output tile at h = 0
+#pragma unroll
+      for (int c = 0; c < NCB; ++c) {
+        float v = accv[c];
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        if (h == 0) acc[0][c][0] += v;
+      }
     }
     __syncthreads();
 
@@ -1158,9 +1205,9 @@ __global__ void __launch_bounds__(256) decode_kernel(const uint32_t* tile_indptr
 }
 
 template <int MB, int MODE, int NCB, bool DENSE, bool SPARSE, int NW, bool SK, int NWS, int XR,
-          bool BK>
+          bool BK, bool DV = false>
 int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stream) {
-  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR, BK>;
+  auto kern = matmul_kernel<MB, MODE, NCB, DENSE, SPARSE, NW, SK, NWS, XR, BK, DV>;
   // the layout of this instance (with no outliers the fused launch drops its
   // sparse half, whose layout is never larger than the plan's)
   const uint32_t lds = lds_layout(MODE, NCB, NW, NWS, XR, SPARSE, pl.slab_M).lds_bytes;
@@ -1190,6 +1237,12 @@ int launch_variant(const fqi::Plan& pl, const MatmulArgs& args, hipStream_t stre
 template <int MB, int MODE, int NCB, int NW, bool SK, int XR, bool BK>
 int launch_roles_bk(const fqi::Plan& pl, const MatmulArgs& a, bool dense, bool sparse,
                     hipStream_t s) {
+  if constexpr (MODE == 1 && MB == 1 && XR == 1 && !SK) {
+    // the dense products on the vector ALUs (plans with DV have no outlier waves)
+    if (pl.DV && dense && sparse)
+      return launch_variant<MB, MODE, NCB, true, true, NW, SK, 0, XR, BK, true>(pl, a, s);
+    if (pl.DV && dense) return launch_variant<MB, MODE, NCB, true, false, NW, SK, 0, XR, BK, true>(pl, a, s);
+  }
   if constexpr (MODE == 1 && !SK && !(NCB == 4 && MB == 2 && NW == 8) && XR < 6) {
     if (dense && sparse && pl.NWS > 0)
       return launch_variant<MB, MODE, NCB, true, true, NW, SK, NW / 2, XR, BK>(pl, a, s);
@@ -1381,6 +1434,12 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   if (N / kTileN > kMaxStrips) return false;
   if (sparse && (B < 1 || B > kMaxBuckets)) return false;
   if ((opts & kOptStrip32) && (opts & (kOptStrip64 | kOptStreamK))) return false;
+  // dense products on the vector ALUs: one row, MFMA outlier mapping,
+  // uniform split-K, no outlier waves
+  if (opts & kOptDenseValu) {
+    if (M != 1 || mode == 0 || (opts & (kOptStreamK | kOptSparseWaves))) return false;
+    mode = 1;
+  }
   Plan p{};
   p.M = M;
   p.K = K;
@@ -1492,6 +1551,7 @@ bool make_plan(int M, int K, int N, int split_k, bool dense, bool sparse, int B,
   // kBulkTiles tiles per dense wave)
   p.BK = dense && !p.stream &&
          ((p.T + p.S - 1) / p.S + p.NW - 1) / p.NW <= fqk::kBulkTiles;
+  p.DV = dense && (opts & kOptDenseValu) ? 1 : 0;
   const fqk::LdsLayout L = fqk::lds_layout(p.MODE, p.NCB, p.NW, p.NWS, p.XS, sparse, p.slab_M);
   p.slot_bytes = L.slot_bytes;
   p.off_xs = L.off_xs;

@@ -263,6 +263,50 @@ def test_exact_group_count_boundaries(gpu_lib, n_groups, M, sparse):
         assert np.array_equal(y, y_ref), (n_groups, M, sparse, f)
 
 
+DENSE_VALU = 128   # FQ_DENSE_VALU
+
+
+@pytest.mark.parametrize("case", [c for c in EXACT_CASES if c[0] == 1],
+                         ids=[f"exact{i}" for i, c in enumerate(EXACT_CASES) if c[0] == 1])
+@pytest.mark.parametrize("strip", [0, 16, 32], ids=["auto", "strip32", "strip64"])
+def test_exact_dense_valu_bit_exact(gpu_lib, case, strip):
+    """The dense products on the vector ALUs (bf16 dot products per lane, the
+    k-chunks summed across lanes after the last tile) instead of MFMA: one
+    row, fused, unfused and dense-only, each strip width, the cases' splits."""
+    M, K, N, frac, split_k, params = case
+    log(f"exact dense-valu M={M} K={K} N={N} frac={frac} split_k={split_k} strip={strip}")
+    prob = make_exact_problem(M, K, N, frac=frac, seed=M * 7 + K + N)
+    f = DENSE_VALU | strip
+    y_ref = ref(prob)
+    for variant in ("fused", "unfused"):
+        y32 = run(gpu_lib, prob, variant, "f32", params, split_k, "mfma", flags=f)
+        assert np.array_equal(y32, y_ref.astype(np.float32)), (variant, np.abs(y32 - y_ref).max())
+    y16 = run(gpu_lib, prob, "fused", "bf16", params, split_k, "mfma", flags=f)
+    assert np.array_equal(y16, oracle.bf16_rne_bits(y_ref))
+    yd = run(gpu_lib, prob, "dense", "f32", split_k=split_k, flags=f)
+    assert np.array_equal(yd, ref(prob, dense_only=True).astype(np.float32))
+
+
+@pytest.mark.parametrize("shape", [(4096, 6144), (4096, 4096), (4096, 28672), (14336, 4096)],
+                         ids=["qkv", "o", "gate_up", "down"])
+def test_full_size_dense_valu_sampled_columns(gpu_lib, shape):
+    """The dense-path ablation at the Llama-3-8B decode shapes, one row, in the
+    launch the benchmark compares with the default: sampled columns against
+    the oracle, and the whole output against the default (MFMA) kernel."""
+    K, N = shape
+    log(f"full dense-valu K={K} N={N}")
+    prob = make_problem(1, K, N, frac=0.01, seed=seed_for(1, FULL_SHAPES.index(shape), 0))
+    rng = np.random.default_rng(K + N + 5)
+    cols = np.unique(np.concatenate([[0, 63, 64, N - 1], rng.choice(N, 192, replace=False)]))
+    y_ref = ref(prob, cols)
+    y16 = run(gpu_lib, prob, "fused", "bf16", flags=DENSE_VALU)
+    assert_bf16_close(y16[:, cols], y_ref)
+    y32 = run(gpu_lib, prob, "fused", "f32", flags=DENSE_VALU)
+    assert_f32_close(y32[:, cols], y_ref)
+    ym = run(gpu_lib, prob, "fused", "f32")
+    assert np.linalg.norm(y32 - ym) / np.linalg.norm(ym) <= F32_FROB
+
+
 def test_exact_dense_only(gpu_lib):
     prob = make_exact_problem(16, 2048, 512, frac=0.02, seed=99)
     y32 = run(gpu_lib, prob, "dense", "f32")

@@ -300,7 +300,11 @@ def _call(lib, pr, X=FAKE, Wq=FAKE, s=FAKE, z=FAKE, tc=None, Y=FAKE, ws=FAKE, ws
     (dict(split_k=-1), "FQ_ERR_SHAPE"),
     (dict(flags=3), "FQ_ERR_UNSUPPORTED"),
     (dict(flags=1, M=5), "FQ_ERR_UNSUPPORTED"),
-    (dict(flags=128), "FQ_ERR_UNSUPPORTED"),
+    (dict(flags=256), "FQ_ERR_UNSUPPORTED"),       # no such switch
+    (dict(flags=128, M=2), "FQ_ERR_UNSUPPORTED"),  # dense products on the VALUs: one row only
+    (dict(flags=128 | 1, M=1), "FQ_ERR_UNSUPPORTED"),    # ... with the MFMA outlier mapping
+    (dict(flags=128 | 4, M=1), "FQ_ERR_UNSUPPORTED"),    # ... uniform split-K
+    (dict(flags=128 | 64, M=1), "FQ_ERR_UNSUPPORTED"),   # ... no outlier waves
     (dict(flags=16 | 32), "FQ_ERR_UNSUPPORTED"),   # both strip widths
     (dict(flags=16 | 4), "FQ_ERR_UNSUPPORTED"),    # 32-column strips with Stream-K
     (dict(flags=16 | 1), "FQ_ERR_UNSUPPORTED"),    # 32-column strips with the gather mapping
@@ -458,6 +462,15 @@ def test_launch_config_switches(lib):
         fq.fq_launch_config(1, 4096, 4096, group_mode=2)
     with pytest.raises(fq.FqError):
         fq.fq_launch_config(5, 4096, 4096, sparse="gather")
+    # the dense-path ablation (VALU dot products) runs the MFMA outlier mapping
+    # in the default shape, at one row only
+    dv = fq.fq_launch_config(1, 4096, 28672, flags=fq.FQ_DENSE_VALU, group_mode=fq.FQ_GROUP_BY_COLUMN)
+    assert dv["mapping"] == "mfma" and dv["x_stage_loads"] == 1
+    base = fq.fq_launch_config(1, 4096, 28672)
+    assert {k: dv[k] for k in ("strip_cols", "split_k", "dense_waves", "workgroups")} == \
+        {k: base[k] for k in ("strip_cols", "split_k", "dense_waves", "workgroups")}
+    with pytest.raises(fq.FqError):
+        fq.fq_launch_config(4, 4096, 4096, flags=fq.FQ_DENSE_VALU)
 
 
 def test_launch_plans_stay_within_kernel_limits(lib):
