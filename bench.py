@@ -1061,6 +1061,32 @@ def dense_path_summary(csv_path, pass_log, timing_log):
     print("\n".join(out))
 
 
+def xcd_probe(torch, dev):
+    """Markdown on stdout: the XCD each workgroup runs on, against workgroup
+    index mod 8 (the placement the matmul kernels' workgroup dealing assumes
+    for L2 sharing), over the grid sizes and workgroup sizes the kernels
+    launch with; three launches each."""
+    from paper_2608_15531_amd import probe
+    out_lines = ["# Workgroup placement on the XCDs", "",
+                 "Command (repo root, MI355X, ROCm 7.2):", "",
+                 "    python3 -u bench.py --xcd-probe > profiles/xcd_placement.md", "",
+                 "`fq_probe_workgroup_xcd` (include/fq_probe.h): each workgroup writes the XCC_ID "
+                 "hardware register.  `round robin` = every workgroup w ran on XCD w mod 8.", "",
+                 "| workgroups | threads | launch | round robin | workgroups per XCD |",
+                 "|---|---|---|---|---|"]
+    for n, th in ((128, 512), (192, 512), (256, 512), (384, 256), (448, 256), (512, 256),
+                  (1024, 256), (4096, 64)):
+        out = torch.full((n,), -1, dtype=torch.int32, device=dev)
+        for rep in range(3):
+            probe.fq_probe_workgroup_xcd(out, n, th)
+            torch.cuda.synchronize()
+            ids = out.cpu().numpy()
+            rr = bool((ids == (np.arange(n) % 8)).all())
+            hist = np.bincount(ids, minlength=8).tolist()
+            out_lines.append(f"| {n} | {th} | {rep} | {'yes' if rr else 'no'} | {hist} |")
+    print("\n".join(out_lines))
+
+
 TRACE_WARM, TRACE_REPS = 2, 6   # replays per case in the kernel-trace pass
 
 
@@ -1210,6 +1236,9 @@ def main():
                     help="no timing: eager launches of the dominant kernel's matmuls over the "
                          "rotated copies, then a plain copy of COPY_CAL_BYTES, for rocprofv3 "
                          "--pmc FETCH_SIZE / WRITE_SIZE collection")
+    ap.add_argument("--xcd-probe", action="store_true",
+                    help="markdown: the XCD each workgroup runs on, for the grid sizes the "
+                         "kernels use")
     ap.add_argument("--pmc-pass-narrow", action="store_true",
                     help="as --pmc-pass, for the 32-column-strip instance of qkv and o at one row")
     ap.add_argument("--dense-path-pass", action="store_true",
@@ -1301,6 +1330,9 @@ def main():
         return
     if args.pmc_pass_large_m:
         pmc_pass_large_m(fq, torch, dev)
+        return
+    if args.xcd_probe:
+        xcd_probe(torch, dev)
         return
     if args.dense_path_pass or args.dense_path_sweep:
         dense_path_pass(fq, torch, dev, timing=args.dense_path_sweep)

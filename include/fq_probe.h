@@ -43,6 +43,22 @@ extern "C" {
 int fq_probe_stream_read(const void* src, size_t bytes, int32_t workgroups, int32_t waves,
                          int32_t loads_in_flight, uint32_t* sink, void* stream);
 
+/*
+ * fq_probe_workgroup_xcd -- enqueue one kernel whose workgroup w writes the
+ * number of the accelerator complex die (XCD, read from the hardware XCC_ID
+ * register) it runs on to out[w].  The matmul kernels deal their workgroups
+ * so that neighbouring output strips share an XCD's L2 under the dispatcher's
+ * round-robin placement; this probe shows the placement that actually
+ * happens.
+ *   out         device pointer to `workgroups` uint32 words (4-byte aligned).
+ *   workgroups  grid size, 1..65536.
+ *   threads     threads per workgroup: 64, 128, 256, 512 or 1024.
+ *   stream      hipStream_t (NULL: the default stream).
+ * Returns 0 on success, 1 on a bad argument (nothing launched), 2 when the
+ * HIP runtime reported a launch error.
+ */
+int fq_probe_workgroup_xcd(uint32_t* out, int32_t workgroups, int32_t threads, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -42,7 +42,26 @@ int launch(const void* src, uint64_t n16, int wgs, int waves, uint32_t* sink, hi
   return hipGetLastError() == hipSuccess ? 0 : 2;
 }
 
+__global__ void __launch_bounds__(1024) workgroup_xcd(uint32_t* out, int n) {
+  if (threadIdx.x == 0 && int(blockIdx.x) < n) {
+    uint32_t id;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(id));
+    out[blockIdx.x] = id & 15u;   // bits 3:0: the XCC number
+  }
+}
+
 }  // namespace
+
+extern "C" int fq_probe_workgroup_xcd(uint32_t* out, int32_t workgroups, int32_t threads,
+                                      void* stream) {
+  if (!out || (reinterpret_cast<uintptr_t>(out) & 3) || workgroups < 1 || workgroups > 65536)
+    return 1;
+  if (threads != 64 && threads != 128 && threads != 256 && threads != 512 && threads != 1024)
+    return 1;
+  hipLaunchKernelGGL(workgroup_xcd, dim3(unsigned(workgroups)), dim3(unsigned(threads)), 0,
+                     static_cast<hipStream_t>(stream), out, workgroups);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
 
 extern "C" int fq_probe_stream_read(const void* src, size_t bytes, int32_t workgroups,
                                     int32_t waves, int32_t loads_in_flight, uint32_t* sink,

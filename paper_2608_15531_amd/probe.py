@@ -10,7 +10,7 @@ import threading
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 PROBE_LIB_PATH = os.path.join(_HERE, "libfqprobe.so")
-EXPORTS = ("fq_probe_stream_read",)
+EXPORTS = ("fq_probe_stream_read", "fq_probe_workgroup_xcd")
 
 _lib = None
 _lock = threading.Lock()
@@ -27,6 +27,8 @@ def load() -> C.CDLL:
             lib.fq_probe_stream_read.argtypes = [C.c_void_p, C.c_size_t, C.c_int32, C.c_int32,
                                                  C.c_int32, C.c_void_p, C.c_void_p]
             lib.fq_probe_stream_read.restype = C.c_int
+            lib.fq_probe_workgroup_xcd.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]
+            lib.fq_probe_workgroup_xcd.restype = C.c_int
             _lib = lib
     return _lib
 
@@ -45,3 +47,16 @@ def fq_probe_stream_read(src, nbytes: int, workgroups: int, waves: int, loads_in
                                      loads_in_flight, sink.data_ptr(), int(stream.cuda_stream))
     if rc != 0:
         raise RuntimeError(f"fq_probe_stream_read failed ({rc})")
+
+
+def fq_probe_workgroup_xcd(out, workgroups: int, threads: int, stream=None) -> None:
+    """Enqueue the XCD-placement probe: out (device int32 tensor of at least
+    `workgroups` words) receives the XCD each workgroup ran on."""
+    import torch
+    if out.numel() * out.element_size() < 4 * workgroups:
+        raise ValueError("fq_probe_workgroup_xcd: buffer too small")
+    if stream is None:
+        stream = torch.cuda.current_stream(out.device)
+    rc = load().fq_probe_workgroup_xcd(out.data_ptr(), workgroups, threads, int(stream.cuda_stream))
+    if rc != 0:
+        raise RuntimeError(f"fq_probe_workgroup_xcd failed ({rc})")

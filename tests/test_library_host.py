@@ -60,6 +60,11 @@ def test_probe_library_exports_its_header(lib):
     assert f(addr, 256, 0, 1, 1, addr, None) == 1                # no workgroups
     assert f(addr, 256, 1, 3, 1, addr, None) == 1                # bad wave count
     assert f(addr, 256, 1, 1, 3, addr, None) == 1                # bad loads in flight
+    x = plib.fq_probe_workgroup_xcd
+    assert x(None, 8, 64, None) == 1                             # null output
+    assert x(addr + 2, 8, 64, None) == 1                         # misaligned output
+    assert x(addr, 0, 64, None) == 1                             # no workgroups
+    assert x(addr, 8, 96, None) == 1                             # bad thread count
 
 
 def test_default_params(lib):
