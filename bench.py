@@ -1061,6 +1061,120 @@ def dense_path_summary(csv_path, pass_log, timing_log):
     print("\n".join(out))
 
 
+TILE_PROBE_SHAPES = [(4096, 28672), (14336, 4096)]
+TILE_PROBE_GPT = 21   # groups per tile: the default packing's mean at 1 % outliers
+
+
+def tile_load_probe(torch, dev, R: int = 4):
+    """Markdown on stdout: the per-tile loads of the fused kernel without its
+    compute (fq_probe_tile_loads), one kind of load added at a time, graph
+    replays over R rotated buffers."""
+    from paper_2608_15531_amd import probe
+    P = probe
+    variants = [("codes only", 0), ("+ scales, zero-points", P.FQ_PROBE_SCALES | P.FQ_PROBE_ZEROS),
+                ("+ X", P.FQ_PROBE_X), ("+ groups", P.FQ_PROBE_GROUPS),
+                ("+ X, groups", P.FQ_PROBE_X | P.FQ_PROBE_GROUPS),
+                ("+ all four", P.FQ_PROBE_SCALES | P.FQ_PROBE_ZEROS | P.FQ_PROBE_X | P.FQ_PROBE_GROUPS),
+                ("+ X, masked to 16 lanes", P.FQ_PROBE_X | P.FQ_PROBE_MASKED),
+                ("+ groups, masked to 21 lanes", P.FQ_PROBE_GROUPS | P.FQ_PROBE_MASKED)]
+    out = ["# Per-tile load cost: the fused kernel's loads without its compute", "",
+           "Command (repo root, MI355X, ROCm 7.2):", "",
+           "    python3 -u bench.py --tile-load-probe > profiles/tile_load_probe.md", "",
+           "`fq_probe_tile_loads` (include/fq_probe.h) issues the loads of the fused kernel's "
+           "tile loop on 64-column strips (four waves per strip, two 128-row tiles in flight per "
+           "wave, four 16-byte code loads per lane and tile) and nothing else; each row adds one "
+           "kind of per-tile load (scales 8 B, zero-point word 4 B, one 16-byte X load, one "
+           f"16-byte Tile-COO group load with {TILE_PROBE_GPT} groups per tile).  Graph replays "
+           f"over {R} rotated buffers; us per launch.  The added bytes are 3-10 % of the codes', "
+           "so a plain bandwidth bound predicts almost no change.", "",
+           "| K x N | loads per tile and lane | us per launch | vs codes only | code MB |",
+           "|---|---|---|---|---|"]
+    for K, N in TILE_PROBE_SHAPES:
+        T = K // 128
+        bufs = []
+        for _ in range(R):
+            bufs.append((torch.zeros(K * N // 8, dtype=torch.int32, device=dev),
+                         torch.zeros(T * N, dtype=torch.int16, device=dev),
+                         torch.zeros(T * N // 8, dtype=torch.int32, device=dev),
+                         torch.zeros(K, dtype=torch.int16, device=dev),
+                         torch.zeros(T * (N // 64) * TILE_PROBE_GPT * 4, dtype=torch.int32,
+                                     device=dev)))
+        sink = torch.zeros(N // 64, dtype=torch.int32, device=dev)
+        base = None
+        for label, extra in variants:
+            L = 8 * R
+            g = capture_graph(torch, lambda: [probe.fq_probe_tile_loads(
+                *bufs[i % R], K, N, TILE_PROBE_GPT, extra, sink) for i in range(L)])
+            us = min(graph_us(torch, g, L, 6), graph_us(torch, g, L, 6))
+            del g
+            base = us if base is None else base
+            out.append(f"| {K}x{N} | {label} | {us:.2f} | {us - base:+.2f} | "
+                       f"{K * N / 2 / 1e6:.1f} |")
+        del bufs
+        torch.cuda.empty_cache()
+    print("\n".join(out))
+
+
+def launch_timeline(torch, dev, R: int = 8):
+    """Markdown on stdout: where a fused launch's time goes, per wave, from the
+    instrumented build (libfq_stamps.so): each Llama-3-8B decode matmul in a
+    graph of 4 R launches over R rotated weight copies, the last launch's
+    stamps after replays, median of 5."""
+    import paper_2608_15531_amd as fq
+    from synth import make_activations, make_problem, seed_for
+    fq.use_instrumented_build()
+    out = ["# Launch timeline of the fused kernel (per-wave timestamps)", "",
+           "Command (repo root, MI355X, ROCm 7.2):", "",
+           "    python3 -u bench.py --launch-timeline > profiles/launch_timeline.md", "",
+           "The instrumented build `libfq_stamps.so` (include/fq_debug.h: the same kernels with "
+           "four `s_memrealtime` stamps per wave) runs each Llama-3-8B decode matmul (default "
+           "packing, 1 % outliers) in a graph of 32 launches over 8 rotated weight copies; after "
+           "warm replays the last launch's stamps are read.  Times in us from the first wave's "
+           "start: `start` = when a wave began (median / max over waves), `first data` = from "
+           "its start until its first tile's loads had arrived, `loop` = its tile loop, "
+           "`epilogue` = from the loop's end to its exit (the workgroup barrier, the reduction "
+           "across waves and, under split-K, across workgroups), `end` = its exit (median / max: "
+           "the max is the kernel's span).  `launch` = HIP-event time per launch of the graph "
+           "(the span plus the dispatch gap).  Medians over 5 replays.", "",
+           "| matmul | waves | launch us | start med / max | first data | loop | epilogue "
+           "(med / p90) | end med / max |", "|---|---|---|---|---|---|---|---|"]
+    ws = torch.zeros(64 << 20, dtype=torch.uint8, device=dev)
+    for si, (name, K, N) in enumerate(SHAPES):
+        p = make_problem(1, K, N, frac=FRAC, seed=seed_for(1, si, 0))
+        host = fq.fq_pack_tile_coo(K, N, p.k, p.n, p.v)
+        W = [fq.to_device(p, dev)[1:] for _ in range(R)]
+        T = [fq.TileCOODevice(host, dev) for _ in range(R)]
+        for mi, M in enumerate(MS):
+            x = torch.from_numpy(make_activations(M, K, seed_for(1, si, mi)).view(np.int16)
+                                 .copy()).view(torch.bfloat16).to(dev)
+            Y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            c = fq.fq_launch_config(M, K, N)
+            nw = c["workgroups"] * (c["dense_waves"] + c["outlier_waves"])
+            L = 4 * R
+            g = capture_graph(torch, lambda: [fq.fq_w4a16_outlier_matmul(
+                x, *W[i % R], T[i % R], Y=Y, ws=ws) for i in range(L)])
+            rows = []
+            for _ in range(5):
+                us = graph_us(torch, g, L, 2)
+                st = fq.fq_debug_wave_stamps(nw).astype(np.int64)
+                t0 = st[:, 0].min()
+                start = (st[:, 0] - t0) / 100.0
+                first = (st[:, 1] - st[:, 0]) / 100.0
+                loop = (st[:, 2] - st[:, 1]) / 100.0
+                epi = (st[:, 3] - st[:, 2]) / 100.0
+                end = (st[:, 3] - t0) / 100.0
+                rows.append([us, np.median(start), start.max(), np.median(first), np.median(loop),
+                             np.median(epi), np.percentile(epi, 90), np.median(end), end.max()])
+            del g
+            m = np.median(np.array(rows), axis=0)
+            out.append(f"| {name}/M{M} | {nw} | {m[0]:.2f} | {m[1]:.2f} / {m[2]:.2f} | "
+                       f"{m[3]:.2f} | {m[4]:.2f} | {m[5]:.2f} / {m[6]:.2f} | "
+                       f"{m[7]:.2f} / {m[8]:.2f} |")
+        del W, T
+        torch.cuda.empty_cache()
+    print("\n".join(out))
+
+
 def xcd_probe(torch, dev):
     """Markdown on stdout: the XCD each workgroup runs on, against workgroup
     index mod 8 (the placement the matmul kernels' workgroup dealing assumes
@@ -1236,6 +1350,10 @@ def main():
                     help="no timing: eager launches of the dominant kernel's matmuls over the "
                          "rotated copies, then a plain copy of COPY_CAL_BYTES, for rocprofv3 "
                          "--pmc FETCH_SIZE / WRITE_SIZE collection")
+    ap.add_argument("--tile-load-probe", action="store_true",
+                    help="markdown: cost of each kind of per-tile load (fq_probe_tile_loads)")
+    ap.add_argument("--launch-timeline", action="store_true",
+                    help="markdown: per-wave launch timeline from the instrumented build")
     ap.add_argument("--xcd-probe", action="store_true",
                     help="markdown: the XCD each workgroup runs on, for the grid sizes the "
                          "kernels use")
@@ -1321,6 +1439,9 @@ def main():
     import paper_2608_15531_amd as fq
     from synth import make_activations, make_problem, seed_for
 
+    if args.launch_timeline:
+        launch_timeline(torch, torch.device("cuda:0"))
+        return
     fq.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -1333,6 +1454,9 @@ def main():
         return
     if args.xcd_probe:
         xcd_probe(torch, dev)
+        return
+    if args.tile_load_probe:
+        tile_load_probe(torch, dev)
         return
     if args.dense_path_pass or args.dense_path_sweep:
         dense_path_pass(fq, torch, dev, timing=args.dense_path_sweep)

@@ -59,6 +59,39 @@ int fq_probe_stream_read(const void* src, size_t bytes, int32_t workgroups, int3
  */
 int fq_probe_workgroup_xcd(uint32_t* out, int32_t workgroups, int32_t threads, void* stream);
 
+/*
+ * fq_probe_tile_loads -- enqueue one kernel that issues the per-tile loads of
+ * the fused matmul (64-column strips, four waves per strip, two 128-row tiles
+ * in flight per wave) without its compute, to measure what each kind of load
+ * costs.  Every tile loads its codes (four 16-byte loads per lane); `extra`
+ * adds, per tile and lane:
+ *   FQ_PROBE_SCALES   the strip's fp16 scales (8 bytes)
+ *   FQ_PROBE_ZEROS    the zero-point word (4 bytes)
+ *   FQ_PROBE_X        one 16-byte X load (the row-wise X load of one row)
+ *   FQ_PROBE_GROUPS   one 16-byte Tile-COO group load (lanes past the tile's
+ *                     groups_per_tile reload its last group)
+ *   FQ_PROBE_MASKED   X and group loads only in the lanes that need them
+ *                     (16 for X, groups_per_tile for the groups)
+ * Accepted combinations: 0, SCALES|ZEROS, X, GROUPS, X|GROUPS,
+ * SCALES|ZEROS|X|GROUPS, X|MASKED, GROUPS|MASKED.
+ *   codes    device uint32 [K/8][N] (16-byte aligned)
+ *   scales   device fp16 [K/128][N] (8-byte aligned)
+ *   zeros    device uint32 [K/128][N/8] (4-byte aligned)
+ *   x        device bf16 [K] (one row; 16-byte aligned)
+ *   groups   device 16-byte groups, groups_per_tile (1..64) per 128 x 64 tile,
+ *            tiles strip-major, (K/128)(N/64) tiles (16-byte aligned)
+ *   K, N     K % 128 == 0, N % 64 == 0, N / 64 <= 65536
+ *   sink     device uint32 [N/64]; contents unspecified after the call
+ *   stream   hipStream_t (NULL: the default stream)
+ * Returns 0 on success, 1 on a bad argument (nothing launched), 2 when the
+ * HIP runtime reported a launch error.
+ */
+enum { FQ_PROBE_SCALES = 1, FQ_PROBE_ZEROS = 2, FQ_PROBE_X = 4, FQ_PROBE_GROUPS = 8,
+       FQ_PROBE_MASKED = 16 };
+int fq_probe_tile_loads(const void* codes, const void* scales, const void* zeros, const void* x,
+                        const void* groups, int32_t K, int32_t N, int32_t groups_per_tile,
+                        uint32_t extra, uint32_t* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -136,6 +136,42 @@ def load() -> C.CDLL:
     return _lib
 
 
+STAMPS_LIB_PATH = os.path.join(os.path.dirname(LIB_PATH), "libfq_stamps.so")
+
+
+def use_instrumented_build() -> C.CDLL:
+    """Switch this process to libfq_stamps.so, the build of the same sources
+    in which every wave of a matmul launch records timestamps
+    (include/fq_debug.h), for measurement only.  Call it before anything else
+    uses the library; raises if that build is missing."""
+    global _lib
+    with _lock:
+        if not os.path.exists(STAMPS_LIB_PATH):
+            raise ImportError(f"libfq_stamps.so is not built ({STAMPS_LIB_PATH})")
+        lib = C.CDLL(STAMPS_LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = res
+        lib.fq_debug_wave_stamps.argtypes = [C.c_void_p, C.c_int64]
+        lib.fq_debug_wave_stamps.restype = C.c_int
+        _lib = lib
+    return _lib
+
+
+def fq_debug_wave_stamps(n_waves: int) -> np.ndarray:
+    """The per-wave timestamps of the last matmul launch (instrumented build
+    only): uint64 [n_waves][4] = start, first tile's data, end of the tile
+    loop, exit, in ticks of the 100 MHz s_memrealtime counter."""
+    lib = load()
+    if not hasattr(lib, "fq_debug_wave_stamps") or lib.fq_debug_wave_stamps.argtypes is None:
+        raise RuntimeError("fq_debug_wave_stamps: call use_instrumented_build() first")
+    out = np.zeros((n_waves, 4), np.uint64)
+    if lib.fq_debug_wave_stamps(out.ctypes.data, n_waves) != 0:
+        raise RuntimeError("fq_debug_wave_stamps failed")
+    return out
+
+
 def _check(status: int, where: str) -> None:
     if status != FQ_OK:
         raise FqError(status, where)

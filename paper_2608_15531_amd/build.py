@@ -18,6 +18,9 @@ LIB_PATH = os.path.join(HERE, LIB_NAME)
 # library of its own
 PROBE_LIB_PATH = os.path.join(HERE, "libfqprobe.so")
 PROBE_SOURCES = ["probe.hip"]
+# the instrumented build (per-wave timestamps, include/fq_debug.h): the same
+# sources with FQ_WAVE_STAMPS defined
+STAMPS_LIB_PATH = os.path.join(HERE, "libfq_stamps.so")
 
 HOST_SOURCES = ["capi.cpp", "tilecoo.cpp", "quant.cpp"]
 HIP_SOURCES = ["kernels.hip"]
@@ -52,8 +55,9 @@ def _run(cmd, verbose):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link libfq.so and libfqprobe.so next to this
-    file; returns the path of libfq.so."""
+    """Compile every source and link libfq.so, libfqprobe.so and the
+    instrumented libfq_stamps.so next to this file; returns the path of
+    libfq.so."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     incs = ["-I", INCLUDE, "-I", CSRC]
     jobs = []
@@ -63,12 +67,20 @@ def build(verbose: bool = False) -> str:
     for src in HIP_SOURCES + PROBE_SOURCES:
         obj = os.path.join(BUILD_DIR, src + ".o")
         jobs.append([_hipcc(), *HIP_FLAGS, *incs, "-c", os.path.join(CSRC, src), "-o", obj])
+    stamp_objs = []
+    for src in HIP_SOURCES:
+        obj = os.path.join(BUILD_DIR, src + ".stamps.o")
+        stamp_objs.append(obj)
+        jobs.append([_hipcc(), *HIP_FLAGS, "-DFQ_WAVE_STAMPS", *incs, "-c", os.path.join(CSRC, src),
+                     "-o", obj])
     with ThreadPoolExecutor(max_workers=4) as ex:
         list(ex.map(lambda c: _run(c, verbose), jobs))
-    objs = [j[-1] for j in jobs]
+    objs = [j[-1] for j in jobs if j[-1] not in stamp_objs]
     probe_objs = [o for o in objs if os.path.basename(o)[:-2] in PROBE_SOURCES]
     lib_objs = [o for o in objs if o not in probe_objs]
-    for path, ob in ((LIB_PATH, lib_objs), (PROBE_LIB_PATH, probe_objs)):
+    host_objs = [o for o in lib_objs if os.path.basename(o)[:-2] in HOST_SOURCES]
+    for path, ob in ((LIB_PATH, lib_objs), (PROBE_LIB_PATH, probe_objs),
+                     (STAMPS_LIB_PATH, host_objs + stamp_objs)):
         tmp = path + ".tmp"
         _run([_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *ob, "-o", tmp], verbose)
         shutil.move(tmp, path)

@@ -61,6 +61,14 @@
 
 namespace fqk {
 
+#ifdef FQ_WAVE_STAMPS
+// Instrumented build (libfq_stamps.so, include/fq_debug.h): every wave of a
+// matmul launch records s_memrealtime (100 MHz) when it starts, when its first
+// tile's data have arrived, when its tile loop ends and when it exits.
+constexpr int kMaxStampWaves = 8192;
+__device__ uint64_t g_wave_stamps[kMaxStampWaves][4];
+#endif
+
 constexpr int kXRow = fqi::kXStride;   // LDS row stride of a staged X slice, elements
 constexpr int kGatherLimitM = fqi::kGatherLimitM;
 
@@ -559,6 +567,10 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
                 "dense dot products: one row, MFMA outlier mapping");
   constexpr int NC = 16 * NCB;                 // strip width, columns
   extern __shared__ __align__(16) unsigned char smem[];
+#ifdef FQ_WAVE_STAMPS
+  const uint64_t stamp0 = __builtin_amdgcn_s_memrealtime();
+  uint64_t stamp1 = 0, stamp2 = 0;
+#endif
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // wave-uniform: keeps the tile loop in scalar control flow
@@ -984,6 +996,9 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
         for (int i = 0; i < D; ++i) {
           if (i == 0 || t + i < w_hi) {
             wait_vmcnt<(D - 1) * NL>();
+#ifdef FQ_WAVE_STAMPS
+            if (stamp1 == 0) stamp1 = __builtin_amdgcn_s_memrealtime();
+#endif
             compute(rg[i], t + i - w_lo);
           }
           issue(min(t + i + D, last), rg[i]);
@@ -1064,6 +1079,9 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
     } else {
       tiles(std::integral_constant<bool, KD>{}, std::integral_constant<bool, KS>{});
     }
+#ifdef FQ_WAVE_STAMPS
+    stamp2 = __builtin_amdgcn_s_memrealtime();
+#endif
     if constexpr (DV) {
       // lanes (h, c4), h = 0..3, hold the four k-chunks of the same columns:
       // sum them (fixed order) into row 0 of the output tile at h = 0
@@ -1177,6 +1195,16 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
     if (!SK) break;
     __syncthreads();   // the next segment reuses LDS
   }
+#ifdef FQ_WAVE_STAMPS
+  const uint64_t stamp3 = __builtin_amdgcn_s_memrealtime();
+  const uint32_t wi = blockIdx.x * uint32_t(NT) + uint32_t(tid >> 6);
+  if (lane == 0 && wi < uint32_t(kMaxStampWaves)) {
+    g_wave_stamps[wi][0] = stamp0;
+    g_wave_stamps[wi][1] = stamp1;
+    g_wave_stamps[wi][2] = stamp2;
+    g_wave_stamps[wi][3] = stamp3;
+  }
+#endif
 }
 
 // Thread per group: decode with the same routine the matmul kernels use and
@@ -1622,3 +1650,13 @@ int launch_decode(const uint32_t* tile_indptr, int64_t n_tiles, const uint32_t* 
 }
 
 }  // namespace fqi
+
+#ifdef FQ_WAVE_STAMPS
+#include "fq_debug.h"
+
+extern "C" int fq_debug_wave_stamps(uint64_t* host, int64_t n_waves) {
+  if (!host || n_waves < 1 || n_waves > fqk::kMaxStampWaves) return 1;
+  return hipMemcpyFromSymbol(host, HIP_SYMBOL(fqk::g_wave_stamps), size_t(n_waves) * 32, 0,
+                             hipMemcpyDeviceToHost) == hipSuccess ? 0 : 2;
+}
+#endif

@@ -50,7 +50,110 @@ __global__ void __launch_bounds__(1024) workgroup_xcd(uint32_t* out, int n) {
   }
 }
 
+// The per-tile loads of the fused kernel on 64-column strips, without its
+// compute: workgroup = strip (N / 64 of them), four waves splitting the strip's
+// K / 128 tiles into contiguous ranges, two tiles in flight per wave (tile t+2
+// is issued when t is consumed; past the last tile a wave re-reads it).  Per
+// tile: four 16-byte code loads per lane (one per 32-row step), and by `extra`
+// the scales (8 B), the zero-point word (4 B), one 16-byte X load and one
+// 16-byte Tile-COO group load per lane, the last two optionally exec-masked
+// to the lanes that need them (16 for X at one row, `gpt` for the groups).
+// The loaded words are folded into a checksum stored almost never.
+template <uint32_t EXTRA>
+__global__ void __launch_bounds__(256) tile_loads(const uint4* __restrict__ codes,
+                                                  const uint2* __restrict__ scales,
+                                                  const uint32_t* __restrict__ zeros,
+                                                  const uint4* __restrict__ x,
+                                                  const uint4* __restrict__ groups, int T, int N,
+                                                  int gpt, uint32_t* sink) {
+  const int G = gridDim.x, b = blockIdx.x;
+  const int strip = (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 4, c4 = lane & 15;
+  const int t_lo = T * wave / 4, t_hi = T * (wave + 1) / 4;
+  const size_t n4 = size_t(N) / 4;   // 16-byte units per packed row
+  uint32_t acc = 0;
+  uint4 w[2][4], xv[2], gv[2];
+  uint2 s[2];
+  uint32_t z[2];
+  auto issue = [&](int t, int i) {
+    t = t < t_hi ? t : t_hi - 1;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) w[i][st] = codes[(size_t(t) * 16 + 4 * st + h) * n4 + strip * 16 + c4];
+    s[i] = uint2{0u, 0u};
+    z[i] = 0u;
+    xv[i] = gv[i] = uint4{0u, 0u, 0u, 0u};
+    if (EXTRA & FQ_PROBE_SCALES) s[i] = scales[(size_t(t) * N + strip * 64) / 4 + c4];
+    if (EXTRA & FQ_PROBE_ZEROS) z[i] = zeros[(size_t(t) * N + strip * 64) / 8 + c4 / 2];
+    const size_t tile = size_t(strip) * T + t;
+    if (EXTRA & FQ_PROBE_X) {
+      if (!(EXTRA & FQ_PROBE_MASKED) || lane < 16) xv[i] = x[size_t(t) * 16 + c4];
+    }
+    if (EXTRA & FQ_PROBE_GROUPS) {
+      if (!(EXTRA & FQ_PROBE_MASKED)) gv[i] = groups[tile * gpt + min(lane, gpt - 1)];
+      else if (lane < gpt) gv[i] = groups[tile * gpt + lane];
+    }
+  };
+  if (t_lo < t_hi) {
+    issue(t_lo, 0);
+    issue(t_lo + 1, 1);
+    for (int t = t_lo; t < t_hi; t += 2) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        if (i == 0 || t + i < t_hi) {
+#pragma unroll
+          for (int st = 0; st < 4; ++st) acc ^= w[i][st].x ^ w[i][st].y ^ w[i][st].z ^ w[i][st].w;
+          acc ^= s[i].x ^ s[i].y ^ z[i] ^ xv[i].x ^ xv[i].w ^ gv[i].x ^ gv[i].w;
+        }
+        issue(t + i + 2, i);
+      }
+    }
+  }
+  if (acc == kNeverStored) sink[b] = acc;
+}
+
+template <uint32_t E>
+int launch_tiles(const void* c, const void* s, const void* z, const void* x, const void* g, int T,
+                 int N, int gpt, uint32_t* sink, hipStream_t st) {
+  hipLaunchKernelGGL(tile_loads<E>, dim3(unsigned(N / 64)), dim3(256), 0, st,
+                     static_cast<const uint4*>(c), static_cast<const uint2*>(s),
+                     static_cast<const uint32_t*>(z), static_cast<const uint4*>(x),
+                     static_cast<const uint4*>(g), T, N, gpt, sink);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
+
 }  // namespace
+
+extern "C" int fq_probe_tile_loads(const void* codes, const void* scales, const void* zeros,
+                                   const void* x, const void* groups, int32_t K, int32_t N,
+                                   int32_t groups_per_tile, uint32_t extra, uint32_t* sink,
+                                   void* stream) {
+  if (!codes || !scales || !zeros || !x || !groups || !sink) return 1;
+  if (K < 128 || K % 128 || N < 64 || N % 64 || N / 64 > 65536) return 1;
+  if (groups_per_tile < 1 || groups_per_tile > 64) return 1;
+  if ((reinterpret_cast<uintptr_t>(codes) | reinterpret_cast<uintptr_t>(x) |
+       reinterpret_cast<uintptr_t>(groups)) & 15)
+    return 1;
+  if ((reinterpret_cast<uintptr_t>(scales) & 7) || (reinterpret_cast<uintptr_t>(zeros) & 3) ||
+      (reinterpret_cast<uintptr_t>(sink) & 3))
+    return 1;
+  const int T = K / 128, gpt = groups_per_tile;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  constexpr uint32_t SZ = FQ_PROBE_SCALES | FQ_PROBE_ZEROS, XG = FQ_PROBE_X | FQ_PROBE_GROUPS;
+  switch (extra) {
+    case 0: return launch_tiles<0>(codes, scales, zeros, x, groups, T, N, gpt, sink, s);
+    case SZ: return launch_tiles<SZ>(codes, scales, zeros, x, groups, T, N, gpt, sink, s);
+    case FQ_PROBE_X: return launch_tiles<FQ_PROBE_X>(codes, scales, zeros, x, groups, T, N, gpt, sink, s);
+    case FQ_PROBE_GROUPS:
+      return launch_tiles<FQ_PROBE_GROUPS>(codes, scales, zeros, x, groups, T, N, gpt, sink, s);
+    case XG: return launch_tiles<XG>(codes, scales, zeros, x, groups, T, N, gpt, sink, s);
+    case SZ | XG: return launch_tiles<SZ | XG>(codes, scales, zeros, x, groups, T, N, gpt, sink, s);
+    case FQ_PROBE_X | FQ_PROBE_MASKED:
+      return launch_tiles<FQ_PROBE_X | FQ_PROBE_MASKED>(codes, scales, zeros, x, groups, T, N, gpt, sink, s);
+    case FQ_PROBE_GROUPS | FQ_PROBE_MASKED:
+      return launch_tiles<FQ_PROBE_GROUPS | FQ_PROBE_MASKED>(codes, scales, zeros, x, groups, T, N, gpt, sink, s);
+    default: return 1;
+  }
+}
 
 extern "C" int fq_probe_workgroup_xcd(uint32_t* out, int32_t workgroups, int32_t threads,
                                       void* stream) {

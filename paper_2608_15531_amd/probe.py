@@ -10,7 +10,8 @@ import threading
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 PROBE_LIB_PATH = os.path.join(_HERE, "libfqprobe.so")
-EXPORTS = ("fq_probe_stream_read", "fq_probe_workgroup_xcd")
+EXPORTS = ("fq_probe_stream_read", "fq_probe_workgroup_xcd", "fq_probe_tile_loads")
+FQ_PROBE_SCALES, FQ_PROBE_ZEROS, FQ_PROBE_X, FQ_PROBE_GROUPS, FQ_PROBE_MASKED = 1, 2, 4, 8, 16
 
 _lib = None
 _lock = threading.Lock()
@@ -29,6 +30,9 @@ def load() -> C.CDLL:
             lib.fq_probe_stream_read.restype = C.c_int
             lib.fq_probe_workgroup_xcd.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p]
             lib.fq_probe_workgroup_xcd.restype = C.c_int
+            lib.fq_probe_tile_loads.argtypes = [C.c_void_p] * 5 + [C.c_int32, C.c_int32, C.c_int32,
+                                                                   C.c_uint32, C.c_void_p, C.c_void_p]
+            lib.fq_probe_tile_loads.restype = C.c_int
             _lib = lib
     return _lib
 
@@ -60,3 +64,22 @@ def fq_probe_workgroup_xcd(out, workgroups: int, threads: int, stream=None) -> N
     rc = load().fq_probe_workgroup_xcd(out.data_ptr(), workgroups, threads, int(stream.cuda_stream))
     if rc != 0:
         raise RuntimeError(f"fq_probe_workgroup_xcd failed ({rc})")
+
+
+def fq_probe_tile_loads(codes, scales, zeros, x, groups, K: int, N: int, groups_per_tile: int,
+                        extra: int, sink, stream=None) -> None:
+    """Enqueue the per-tile load probe (see include/fq_probe.h) on device
+    tensors; sink: device tensor of at least N / 64 int32 words."""
+    import torch
+    if (codes.numel() * codes.element_size() < K * N // 2
+            or sink.numel() * sink.element_size() < 4 * (N // 64)
+            or groups.numel() * groups.element_size() < 16 * groups_per_tile * (K // 128) * (N // 64)
+            or x.numel() * x.element_size() < 2 * K):
+        raise ValueError("fq_probe_tile_loads: buffer too small")
+    if stream is None:
+        stream = torch.cuda.current_stream(codes.device)
+    rc = load().fq_probe_tile_loads(codes.data_ptr(), scales.data_ptr(), zeros.data_ptr(),
+                                    x.data_ptr(), groups.data_ptr(), K, N, groups_per_tile,
+                                    extra, sink.data_ptr(), int(stream.cuda_stream))
+    if rc != 0:
+        raise RuntimeError(f"fq_probe_tile_loads failed ({rc})")

@@ -60,11 +60,39 @@ def test_probe_library_exports_its_header(lib):
     assert f(addr, 256, 0, 1, 1, addr, None) == 1                # no workgroups
     assert f(addr, 256, 1, 3, 1, addr, None) == 1                # bad wave count
     assert f(addr, 256, 1, 1, 3, addr, None) == 1                # bad loads in flight
+    t = plib.fq_probe_tile_loads
+    assert t(addr, addr, addr, addr, None, 128, 64, 21, 0, addr, None) == 1      # null groups
+    assert t(addr, addr, addr, addr, addr, 100, 64, 21, 0, addr, None) == 1      # K % 128
+    assert t(addr, addr, addr, addr, addr, 128, 96, 21, 0, addr, None) == 1      # N % 64
+    assert t(addr, addr, addr, addr, addr, 128, 64, 65, 0, addr, None) == 1      # > 64 groups
+    assert t(addr, addr, addr, addr, addr, 128, 64, 21, 32, addr, None) == 1     # no such load
+    assert t(addr, addr, addr, addr, addr, 128, 64, 21, 1, addr, None) == 1      # scales alone
+    assert t(addr + 8, addr, addr, addr, addr, 128, 64, 21, 0, addr, None) == 1  # codes misaligned
     x = plib.fq_probe_workgroup_xcd
     assert x(None, 8, 64, None) == 1                             # null output
     assert x(addr + 2, 8, 64, None) == 1                         # misaligned output
     assert x(addr, 0, 64, None) == 1                             # no workgroups
     assert x(addr, 8, 96, None) == 1                             # bad thread count
+
+
+def test_instrumented_build_exports(lib):
+    """libfq_stamps.so, the build with per-wave timestamps, exports every entry
+    point of include/fq.h and what include/fq_debug.h declares, and rejects
+    bad arguments of the stamp reader on the host."""
+    path = fq.STAMPS_LIB_PATH
+    assert os.path.exists(path)
+    slib = C.CDLL(path)
+    for name in fq.EXPORTS:
+        assert getattr(slib, name) is not None
+    with open(os.path.join(ROOT, "include", "fq_debug.h")) as f:
+        declared = set(re.findall(r"^\s*int\s+(fq_\w+)\(", f.read(), re.M))
+    assert declared == {"fq_debug_wave_stamps"}
+    f = slib.fq_debug_wave_stamps
+    f.argtypes = [C.c_void_p, C.c_int64]
+    buf = (C.c_uint64 * 4)()
+    assert f(None, 1) == 1
+    assert f(C.addressof(buf), 0) == 1
+    assert f(C.addressof(buf), 8193) == 1
 
 
 def test_default_params(lib):
