@@ -899,16 +899,35 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
         }
         __builtin_amdgcn_wave_barrier();
         const uint4* b4 = reinterpret_cast<const uint4*>(bo);
+        if constexpr (MB == 1) {
+          // every block of the image is read before the first of its MFMAs,
+          // so the wave waits for the LDS once per tile rather than once per
+          // pair of reads (the compiler's own order); two 16-row blocks keep
+          // the per-step reads, for which the extra registers would spill
+          bf16x8_t Bo[4][NCB];
   #pragma unroll
-        for (int step = 0; step < 4; ++step) {
-          bf16x8_t Bo[NCB];
+          for (int step = 0; step < 4; ++step)
   #pragma unroll
-          for (int c = 0; c < NCB; ++c) Bo[c] = __builtin_bit_cast(bf16x8_t, b4[(step * NCB + c) * 64 + lane]);
+            for (int c = 0; c < NCB; ++c)
+              Bo[step][c] = __builtin_bit_cast(bf16x8_t, b4[(step * NCB + c) * 64 + lane]);
+          __builtin_amdgcn_sched_barrier(0);
   #pragma unroll
-          for (int c = 0; c < NCB; ++c)
+          for (int step = 0; step < 4; ++step)
   #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-              acc[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bo[c], acc[mb][c], 0, 0, 0);
+            for (int c = 0; c < NCB; ++c)
+              acc[0][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[0][step], Bo[step][c], acc[0][c], 0, 0, 0);
+        } else {
+  #pragma unroll
+          for (int step = 0; step < 4; ++step) {
+            bf16x8_t Bo[NCB];
+  #pragma unroll
+            for (int c = 0; c < NCB; ++c) Bo[c] = __builtin_bit_cast(bf16x8_t, b4[(step * NCB + c) * 64 + lane]);
+  #pragma unroll
+            for (int c = 0; c < NCB; ++c)
+  #pragma unroll
+              for (int mb = 0; mb < MB; ++mb)
+                acc[mb][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mb][step], Bo[c], acc[mb][c], 0, 0, 0);
+          }
         }
       }
 
