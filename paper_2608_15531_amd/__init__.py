@@ -535,6 +535,16 @@ def fq_workspace_bytes(M: int, K: int, N: int, y_dtype=FQ_Y_BF16, split_k: int =
     return need.value
 
 
+def fq_workspace_bytes_unfused(M: int, K: int, N: int, y_dtype=FQ_Y_BF16, split_k: int = 0,
+                               group: int = 128, flags: int = 0) -> int:
+    lib = load()
+    pr = _problem(M, K, N, y_dtype, split_k, group, flags=flags)
+    need = C.c_size_t(0)
+    _check(lib.fq_workspace_bytes_unfused(C.byref(pr), C.byref(need)),
+           "fq_workspace_bytes_unfused")
+    return need.value
+
+
 # ---------------------------------------------------- numpy -> device --
 
 def to_device(problem, device="cuda"):

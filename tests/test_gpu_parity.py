@@ -397,15 +397,21 @@ def test_workspace_counters_rearmed(gpu_lib):
     prob = make_problem(4, 4096, 4096, frac=0.01, seed=8)
     X, Wq, s, z = fq.to_device(prob)
     tc = fq.TileCOODevice(fq.fq_pack_tile_coo(4096, 4096, prob.k, prob.n, prob.v))
-    need = fq.fq_workspace_bytes(4, 4096, 4096)
-    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
-    y1 = fq.fq_w4a16_outlier_matmul(X, Wq, s, z, tc, ws=ws)
-    torch.cuda.synchronize()
-    # the counter region (first 256 KiB) is back to zero after the call
-    assert int(ws[:256 * 1024].count_nonzero()) == 0
-    y2 = fq.fq_w4a16_outlier_matmul(X, Wq, s, z, tc, ws=ws)
-    torch.cuda.synchronize()
-    assert torch.equal(y1, y2)
+    for split_k in (0, 4):
+        need = fq.fq_workspace_bytes_unfused(4, 4096, 4096, split_k=split_k)
+        ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+        y1 = fq.fq_w4a16_outlier_matmul(X, Wq, s, z, tc, ws=ws, split_k=split_k)
+        torch.cuda.synchronize()
+        # the counter region (first 256 KiB) is back to zero after the call
+        assert int(ws[:256 * 1024].count_nonzero()) == 0, split_k
+        y2 = fq.fq_w4a16_outlier_matmul(X, Wq, s, z, tc, ws=ws, split_k=split_k)
+        torch.cuda.synchronize()
+        assert torch.equal(y1, y2)
+        # and after the unfused entry point's two kernels, which share it
+        y3 = fq.fq_w4a16_outlier_matmul_unfused(X, Wq, s, z, tc, ws=ws, split_k=split_k)
+        torch.cuda.synchronize()
+        assert int(ws[:256 * 1024].count_nonzero()) == 0, split_k
+        assert_bf16_close(y3.view(torch.int16).cpu().numpy().view(np.uint16), ref(prob))
 
 
 def test_workspace_shared_across_shapes(gpu_lib):
