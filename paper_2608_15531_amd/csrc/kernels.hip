@@ -499,6 +499,32 @@ __device__ __forceinline__ void image_offsets(uint32_t R, uint32_t C, uint32_t& 
   o23 = __builtin_amdgcn_perm(hi, lo, 0x07030602u) << 1;
 }
 
+// The same slots as full LDS byte addresses, for images that lie below
+// 64 KB of LDS at a 256-byte-aligned base: the byte-lane assembly builds byte
+// offsets (the bit layouts above shifted up by one) and ORs the base's high
+// byte, replicated in `base_rep`, into the high bytes, where its bits lie
+// above the offset's.  Each 16-bit half is then a whole address.
+template <int NCB>
+__device__ __forceinline__ void image_addresses(uint32_t R, uint32_t C, uint32_t base_rep,
+                                                uint32_t& a01, uint32_t& a23) {
+  const uint32_t r1 = R >> 1, r3 = R >> 3;
+  uint32_t lo = r1 & 0x02020202u;                 // k2
+  lo = and_or(R << 2, 0x0C0C0C0Cu, lo);           // k0, k1
+  uint32_t hi = and_or(r3, 0x03030303u, base_rep);   // k3, k4
+  if constexpr (NCB == 4) {
+    const uint32_t c2 = C << 2;
+    lo = and_or(c2, 0xF0F0F0F0u, lo);             // n'2..n'5
+    hi = and_or(c2, 0x0C0C0C0Cu, hi);             // n'0, n'1
+    hi = and_or(r1, 0x30303030u, hi);             // k5, k6
+  } else {
+    lo = and_or(C << 3, 0xF0F0F0F0u, lo);         // n'1..n'4
+    hi = and_or(C << 2, 0x04040404u, hi);         // n'0
+    hi = and_or(R >> 2, 0x18181818u, hi);         // k5, k6
+  }
+  a01 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
+  a23 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
+}
+
 typedef __attribute__((address_space(3))) uint16_t lds_u16;
 
 // 16-bit LDS store at an absolute LDS byte address.
@@ -518,17 +544,38 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
 // another group, and so does a slot whose column lies in the other half of a
 // 64-column Tile-COO tile when the strip is 32 columns wide (`half` = which
 // half this strip is; bit 5 of a column selects the half).
-template <int NCB>
+// With FA the addresses come whole from image_addresses (`img` then holds
+// the replicated base byte instead of the base).
+template <int NCB, bool FA>
+__device__ __forceinline__ void group_addresses(uint32_t img, uint32_t R, uint32_t C,
+                                                uint32_t o[4]) {
+  uint32_t o01, o23;
+  if constexpr (FA) {
+    image_addresses<NCB>(R, C, img, o01, o23);
+    o[0] = o01 & 0xFFFFu;
+    o[1] = o01 >> 16;
+    o[2] = o23 & 0xFFFFu;
+    o[3] = o23 >> 16;
+  } else {
+    image_offsets<NCB>(R, C, o01, o23);
+    o[0] = img + (o01 & 0xFFFFu);
+    o[1] = img + (o01 >> 16);
+    o[2] = img + (o23 & 0xFFFFu);
+    o[3] = img + (o23 >> 16);
+  }
+}
+
+template <int NCB, bool FA>
 __device__ __forceinline__ void scatter_group(uint32_t img, uint32_t trash, uint4 raw,
                                               uint32_t half, uint32_t addr[4]) {
-  uint32_t o01, o23;
-  image_offsets<NCB>(raw.x, raw.y, o01, o23);
+  uint32_t o[4];
+  group_addresses<NCB, FA>(img, raw.x, raw.y, o);
   // per slot: bit 5 of its column equals `half` (always true for NCB = 4)
   const uint32_t other = NCB == 4 ? 0u : ((raw.y >> 5) ^ (half * 0x01010101u)) & 0x01010101u;
-  addr[0] = (raw.z & 0xFFFFu) != 0u && !(other & 0x1u) ? img + (o01 & 0xFFFFu) : trash;
-  addr[1] = raw.z > 0xFFFFu && !(other & 0x100u) ? img + (o01 >> 16) : trash;
-  addr[2] = (raw.w & 0xFFFFu) != 0u && !(other & 0x10000u) ? img + (o23 & 0xFFFFu) : trash;
-  addr[3] = raw.w > 0xFFFFu && !(other & 0x1000000u) ? img + (o23 >> 16) : trash;
+  addr[0] = (raw.z & 0xFFFFu) != 0u && !(other & 0x1u) ? o[0] : trash;
+  addr[1] = raw.z > 0xFFFFu && !(other & 0x100u) ? o[1] : trash;
+  addr[2] = (raw.w & 0xFFFFu) != 0u && !(other & 0x10000u) ? o[2] : trash;
+  addr[3] = raw.w > 0xFFFFu && !(other & 0x1000000u) ? o[3] : trash;
   lds_store16(addr[0], raw.z);
   lds_store16(addr[1], raw.z >> 16);
   lds_store16(addr[2], raw.w);
@@ -692,6 +739,12 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       op.lx[mb] = (uint32_t(min(mb * 16 + c4, a.M - 1)) * uint32_t(a.K) + 8u * uint32_t(h)) * 2u;
   }
   const uint32_t img = lds_address(bo);                  // this wave's image
+  // Images below 64 KB of LDS (each at a multiple of its own 4 or 8 KB size,
+  // dynamic LDS starting at 0): the scatter forms whole addresses with the
+  // base's high byte ORed in (image_addresses).
+  constexpr bool kFastAddr =
+      MODE == 1 && uint32_t(NWS > 0 ? NWS : NW) * (uint32_t(fqi::kImageBytes) / 4 * NCB) <= 65536u;
+  const uint32_t img_a = kFastAddr ? (img >> 8) * 0x01010101u : img;
   // X stage of this wave (4 XR rows x 256 bytes, 16-byte chunk q of row r at
   // position q ^ (r mod 16)).  With one 16-row block it has a place of its
   // own, whose first 16 bytes double as the trash word, written by the
@@ -892,10 +945,10 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
       if (SPM) {
   #pragma unroll
         for (int j = 0; j < kGroupLoads; ++j)
-          if (n_g > 64u * j) scatter_group<NCB>(img, trash, cur.g[j], half, addr[j]);
+          if (n_g > 64u * j) scatter_group<NCB, kFastAddr>(img_a, trash, cur.g[j], half, addr[j]);
         for (uint32_t gi = 64 * kGroupLoads + lane; gi < n_g; gi += 64) {
           uint32_t ad[4];
-          scatter_group<NCB>(img, trash, a.packed[cur.g0 + gi], half, ad);
+          scatter_group<NCB, kFastAddr>(img_a, trash, a.packed[cur.g0 + gi], half, ad);
         }
         __builtin_amdgcn_wave_barrier();
         const uint4* b4 = reinterpret_cast<const uint4*>(bo);
@@ -949,11 +1002,9 @@ __global__ void __launch_bounds__(64 * (NW + NWS))
         for (int j = 0; j < kGroupLoads; ++j)
           if (n_g > 64u * j) clear_group(addr[j]);
         for (uint32_t gi = 64 * kGroupLoads + lane; gi < n_g; gi += 64) {
-          uint32_t o01, o23;
           const uint4 raw = a.packed[cur.g0 + gi];
-          image_offsets<NCB>(raw.x, raw.y, o01, o23);
-          const uint32_t ad[4] = {img + (o01 & 0xFFFFu), img + (o01 >> 16), img + (o23 & 0xFFFFu),
-                                  img + (o23 >> 16)};
+          uint32_t ad[4];
+          group_addresses<NCB, kFastAddr>(img_a, raw.x, raw.y, ad);
           clear_group(ad);   // zeros everywhere the group could have written
         }
       }
