@@ -48,6 +48,9 @@ PAPER_TILECOO = {"group_mode": 0, "buckets_per_tile": 16}
 PROBE_CONFIGS = [(256, 8, 4), (512, 4, 4), (512, 8, 2), (1024, 4, 2), (1024, 4, 4),
                  (2048, 4, 2)]
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fused_llama3_8b_decode_traffic.md")
+# bf16 GEMM comparator: candidates per weight layout and workspace limit
+GEMM_CANDIDATES = 16
+GEMM_WORKSPACE = 64 << 20
 
 
 def kernel_name(fq, M, K, N, packing=None, flags=0):
@@ -161,6 +164,75 @@ class StreamProbe:
         del bufs
         self.cache[nbytes] = best
         return best
+
+
+class GemmComparator:
+    """The bf16 GEMM comparator (libfqgemm, include/fq_gemm_ref.h): hipBLASLt
+    on a dense bf16 weight of the same K x N, fp32 accumulation, bf16 Y.  For
+    each (M, K, N) every candidate hipBLASLt's heuristic offers (up to
+    GEMM_CANDIDATES, in both weight layouts: [K][N] and the linear-layer
+    [N][K]) is timed over rotated weight copies in the graph-replay harness,
+    and the fastest is kept, after a check of its output against
+    torch.matmul in fp32."""
+
+    LAYOUTS = ("kn", "nk")
+
+    def __init__(self, torch, dev, source=None, max_candidates=None):
+        from paper_2608_15531_amd import gemm_ref
+        self.torch, self.dev, self.g = torch, dev, gemm_ref
+        self.source = gemm_ref.HEURISTIC if source is None else source
+        self.max_c = max_candidates or GEMM_CANDIDATES
+        self.ws = torch.empty(GEMM_WORKSPACE, dtype=torch.uint8, device=dev)
+
+    def weights(self, K, N, copies):
+        return [self.torch.randn(K * N, device=self.dev, dtype=self.torch.bfloat16)
+                for _ in range(copies)]
+
+    def _launches(self, x, Ws, y, layout, i):
+        K, N = x.shape[1], y.shape[1]
+        shape = (K, N) if layout == "kn" else (N, K)
+        return lambda: [self.g.gemm(x, W.view(shape), y, layout, i, self.ws) for W in Ws]
+
+    def search(self, M, K, N, Ws, reps):
+        """Times every candidate; returns a dict with the fastest one's
+        per-launch us, layout, kernel name and check, the number timed and
+        the us of hipBLASLt's own first choice in the [K][N] layout."""
+        torch, g = self.torch, self.g
+        x = torch.randn(M, K, device=self.dev, dtype=torch.bfloat16)
+        y = torch.empty(M, N, device=self.dev, dtype=torch.bfloat16)
+        timed = []
+        for layout in self.LAYOUTS:
+            n = g.prepare(M, K, N, layout, self.source, self.max_c, GEMM_WORKSPACE)
+            for i in range(n):
+                _, name = g.candidate(M, K, N, layout, i)
+                gr = capture_graph(torch, self._launches(x, Ws, y, layout, i))
+                for _ in range(2):
+                    gr.replay()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(4):
+                    gr.replay()
+                e1.record()
+                torch.cuda.synchronize()
+                timed.append((e0.elapsed_time(e1) * 1e3 / (4 * len(Ws)), layout, i, name))
+                del gr
+        first = next(t for t in timed if t[1] == "kn" and t[2] == 0)
+        _, layout, i, name = min(timed)
+        gr = capture_graph(torch, self._launches(x, Ws, y, layout, i))
+        us = graph_us(torch, gr, len(Ws), reps)
+        del gr
+        # the kept candidate computes the product: Y against fp32 torch.matmul
+        W0 = Ws[0].view((K, N) if layout == "kn" else (N, K))
+        g.gemm(x, W0, y, layout, i, self.ws)
+        ref = x.float() @ (W0.float() if layout == "kn" else W0.float().t())
+        # bf16 rounding of Y plus fp32 accumulation in any order
+        mag = x.float().abs() @ (W0.float().abs() if layout == "kn" else W0.float().abs().t())
+        err = (y.float() - ref).abs() - (2.0 ** -8 * ref.abs() + 2.0 ** -14 * mag)
+        if bool((err > 0).any()) or not bool(torch.isfinite(y).all()):
+            raise RuntimeError(f"bf16 GEMM comparator {name} ({layout}) differs from torch.matmul")
+        return {"us": us, "layout": layout, "index": i, "kernel": name, "candidates": len(timed),
+                "heuristic_first_us": first[0], "heuristic_first_kernel": first[3]}
 
 
 def cpu_model():
@@ -1202,15 +1274,33 @@ def xcd_probe(torch, dev):
 
 
 TRACE_WARM, TRACE_REPS = 2, 6   # replays per case in the kernel-trace pass
+GEMM_TRACE_CALLS = 8            # eager comparator calls per case in that pass
 
 
 def trace_pass(fq, torch, order, launch, R, dev):
     """For a rocprofv3 --kernel-trace run: each (shape, M) fused matmul alone,
     a graph of 4R launches over the rotated copies replayed a fixed number of
-    times, in step order; then the bf16 GEMM comparator (torch.matmul on
-    hipBLASLt) of each shape at M = 1 and 16.  One JSON line names the
+    times, in step order; then the bf16 GEMM comparator (hipBLASLt through
+    libfqgemm, the candidate its search keeps; the search runs before the
+    fused cases) of each shape at M = 1 and 16, GEMM_TRACE_CALLS eager calls
+    each with a synchronisation between cases.  One JSON line names the
     sequence, so the trace splits per matmul (--trace-per-matmul)."""
-    torch.backends.cuda.preferred_blas_library("cublaslt")
+    comp = GemmComparator(torch, dev)
+    gemm, operands = [], []
+    for name, K, N in SHAPES:
+        Ws = comp.weights(K, N, 2)
+        for M in (1, 16):
+            best = comp.search(M, K, N, Ws, 2)
+            gemm.append({"case": f"{name}/M{M}", "M": M, "K": K, "N": N, "layout": best["layout"],
+                         "kernel": best["kernel"], "index": best["index"],
+                         "bytes": 2 * K * N + 2 * M * K + 2 * M * N})
+            # operands made now, so that only the comparator's kernels run
+            # after the fused cases
+            operands.append((Ws[0].view((K, N) if best["layout"] == "kn" else (N, K)),
+                             torch.randn(M, K, device=dev, dtype=torch.bfloat16),
+                             torch.empty(M, N, device=dev, dtype=torch.bfloat16)))
+        del Ws
+    torch.cuda.synchronize()
     L = 4 * R
     seq = []
     for c in order:
@@ -1222,21 +1312,15 @@ def trace_pass(fq, torch, order, launch, R, dev):
                     "bytes": c.bytes, "launches": L * (1 + TRACE_WARM + TRACE_REPS),
                     "untimed": L * (1 + TRACE_WARM)})
         del g
-    gemm = []
-    for name, K, N in SHAPES:
-        W = torch.randn(K, N, device=dev, dtype=torch.bfloat16)
-        for M in (1, 16):
-            x = torch.randn(M, K, device=dev, dtype=torch.bfloat16)
-            out = torch.empty(M, N, device=dev, dtype=torch.bfloat16)
-            torch.cuda.synchronize()
-            for _ in range(8):
-                torch.matmul(x, W, out=out)
-            torch.cuda.synchronize()
-            gemm.append(f"{name}/M{M}")
-        del W
+    for e, (W, x, y) in zip(gemm, operands):
+        # each (M, K, N) was prepared once, by its search: the index still holds
+        for _ in range(GEMM_TRACE_CALLS):
+            comp.g.gemm(x, W, y, e["layout"], e["index"], comp.ws)
+        torch.cuda.synchronize()
+    del operands
     # prelude: main() launches every case once eagerly before this pass
-    print(json.dumps({"trace_pass": seq, "gemm": gemm, "prelude": len(order),
-                      "blas": str(torch.backends.cuda.preferred_blas_library())}), flush=True)
+    print(json.dumps({"trace_pass": seq, "gemm": gemm, "gemm_calls": GEMM_TRACE_CALLS,
+                      "prelude": len(order)}), flush=True)
 
 
 def trace_per_matmul(trace_csv, log_path):
@@ -1300,18 +1384,36 @@ def trace_per_matmul(trace_csv, log_path):
         b = sum(x[0]["bytes"] * x[2] for x in lst) / n
         out.append(f"| `{k}` | {', '.join(x[0]['case'] for x in lst)} | {t:.3f} | {b:.0f} | "
                    f"{b / t / 1e3 / HBM_PEAK_GBS:.3f} |")
+    # the comparator's dispatches after the last fused one, in start order:
+    # each case runs gemm_calls calls of its kept kernel; any other dispatch
+    # (a library call may add a helper kernel) is counted with the case whose
+    # calls it precedes or falls between
     last_fused = int(fused[-1]["End_Timestamp"])
-    gk = {}
-    for r in rows:
-        if int(r["Start_Timestamp"]) > last_fused and "matmul_kernel" not in r["Kernel_Name"]:
-            k = r["Kernel_Name"].split("(")[0][:120]
-            gk.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
-    out += ["", f"bf16 GEMM comparator (torch.matmul, preferred BLAS {meta['blas']}; cases "
-                f"{', '.join(meta['gemm'])}, 8 eager calls each, randn operands): kernels "
-                "launched after the fused matmuls:", "",
-            "| kernel | dispatches | mean us |", "|---|---|---|"]
-    for k, v in sorted(gk.items(), key=lambda kv: -len(kv[1])):
-        out.append(f"| `{k}` | {len(v)} | {np.mean(v) / 1e3:.2f} |")
+    rest = sorted((r for r in rows if int(r["Start_Timestamp"]) > last_fused),
+                  key=lambda r: int(r["Start_Timestamp"]))
+    calls = meta["gemm_calls"]
+    out += ["", "bf16 GEMM comparator: hipBLASLt through libfqgemm (include/fq_gemm_ref.h), the "
+                "candidate its search kept (fastest of the heuristic candidates in the [K][N] and "
+                f"[N][K] weight layouts), {calls} eager calls per case after the fused matmuls; "
+                "kernel-only durations from the same trace.  Bytes: bf16 W, X and Y.", "",
+            "| matmul | layout | kernel | calls | median us | other dispatches | bytes | "
+            "GB/s (median) |", "|---|---|---|---|---|---|---|---|"]
+    j = 0
+    for e in meta["gemm"]:
+        own, others = [], 0
+        while len(own) < calls and j < len(rest):
+            r = rest[j]
+            j += 1
+            if r["Kernel_Name"].split("(")[0].strip() == e["kernel"]:
+                own.append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+            else:
+                others += 1
+        if len(own) < calls:
+            raise SystemExit(f"{e['case']}: {len(own)} dispatches of {e['kernel']} in the trace, "
+                             f"expected {calls}")
+        med = float(np.median(own)) / 1e3
+        out.append(f"| {e['case']} | {e['layout']} | `{e['kernel'][:110]}` | {calls} | "
+                   f"{med:.3f} | {others} | {e['bytes']} | {e['bytes'] / med / 1e3:.0f} |")
     print("\n".join(out))
 
 
@@ -1626,24 +1728,34 @@ def main():
     del probe
 
     if not args.no_compare:
-        # bf16 GEMM comparator: torch.matmul on hipBLASLt with a dense bf16 W
-        # of the same shape (its kernel names: the kernel-trace pass).
+        # bf16 GEMM comparator: hipBLASLt called directly (libfqgemm), the
+        # fastest of its heuristic candidates in both weight layouts; and
+        # torch.matmul on the same weight for reference.
+        comp = GemmComparator(torch, dev)
         for si, (name, K, N) in enumerate(SHAPES):
             copies = max(2, min(R, int(2.2e9 // (2 * K * N))))
-            Ws = [torch.randn(K, N, device=dev, dtype=torch.bfloat16) for _ in range(copies)]
+            Ws = comp.weights(K, N, copies)
             for d in details:
                 if d["shape"] != name:
                     continue
-                x = torch.randn(d["M"], K, device=dev, dtype=torch.bfloat16)
-                out = torch.empty(d["M"], N, device=dev, dtype=torch.bfloat16)
-                g = capture(lambda: [torch.matmul(x, W, out=out) for W in Ws])
-                us = graph_us(torch, g, copies, reps)
-                d["bf16_gemm_us"] = round(us, 3)
-                # the GEMM's own algorithmic bytes: bf16 W, X and Y
-                d["bf16_gemm_GBs"] = round((2 * K * N + 2 * d["M"] * K + 2 * d["M"] * N) / us / 1e3, 1)
-                d["speedup_vs_bf16_gemm"] = round(us / d["fused_us"], 3)
+                M = d["M"]
+                best = comp.search(M, K, N, Ws, reps)
+                gemm_bytes = 2 * K * N + 2 * M * K + 2 * M * N   # bf16 W, X and Y
+                d["bf16_gemm_us"] = round(best["us"], 3)
+                d["bf16_gemm_GBs"] = round(gemm_bytes / best["us"] / 1e3, 1)
+                d["bf16_gemm_kernel"] = best["kernel"]
+                d["bf16_gemm_layout"] = best["layout"]
+                d["bf16_gemm_candidates"] = best["candidates"]
+                d["bf16_gemm_heuristic_first_us"] = round(best["heuristic_first_us"], 3)
+                d["speedup_vs_bf16_gemm"] = round(best["us"] / d["fused_us"], 3)
+                x = torch.randn(M, K, device=dev, dtype=torch.bfloat16)
+                out = torch.empty(M, N, device=dev, dtype=torch.bfloat16)
+                g = capture(lambda: [torch.matmul(x, W.view(K, N), out=out) for W in Ws])
+                d["torch_matmul_us"] = round(graph_us(torch, g, copies, reps), 3)
+                del g
             del Ws
             torch.cuda.empty_cache()
+        del comp
 
     # Dominant kernel: the fused kernel instance that moves most of the
     # step's bytes; the other launches are reported beside it.
@@ -1706,7 +1818,11 @@ def main():
         },
         "layer_aggregate": layers,
         "tilecoo_paper_format": paper_step,
-        "bf16_gemm_comparator": f"torch.matmul on {blas} (hipBLASLt), bf16 K x N weight",
+        "bf16_gemm_comparator": "hipBLASLt called directly (libfqgemm): bf16 K x N weight, "
+                                "fp32 accumulation, bf16 Y; fastest of up to "
+                                f"{GEMM_CANDIDATES} heuristic candidates in each of the [K][N] "
+                                "and [N][K] weight layouts; torch_matmul_us: torch.matmul "
+                                f"on {blas}",
         "per_matmul": details,
         "pack_s": {k: round(v, 3) for k, v in pack_s.items()},
     }

@@ -21,6 +21,11 @@ PROBE_SOURCES = ["probe.hip"]
 # the instrumented build (per-wave timestamps, include/fq_debug.h): the same
 # sources with FQ_WAVE_STAMPS defined
 STAMPS_LIB_PATH = os.path.join(HERE, "libfq_stamps.so")
+# the bf16 GEMM comparator on hipBLASLt (include/fq_gemm_ref.h): host code
+# only, a library of its own
+GEMM_LIB_PATH = os.path.join(HERE, "libfqgemm.so")
+GEMM_SOURCES = ["gemm_ref.cpp"]
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 HOST_SOURCES = ["capi.cpp", "tilecoo.cpp", "quant.cpp"]
 HIP_SOURCES = ["kernels.hip"]
@@ -55,15 +60,19 @@ def _run(cmd, verbose):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link libfq.so, libfqprobe.so and the
-    instrumented libfq_stamps.so next to this file; returns the path of
-    libfq.so."""
+    """Compile every source and link libfq.so, libfqprobe.so, the
+    instrumented libfq_stamps.so and the comparator libfqgemm.so next to this
+    file; returns the path of libfq.so."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     incs = ["-I", INCLUDE, "-I", CSRC]
     jobs = []
     for src in HOST_SOURCES:
         obj = os.path.join(BUILD_DIR, src + ".o")
         jobs.append(["g++", *HOST_FLAGS, *incs, "-c", os.path.join(CSRC, src), "-o", obj])
+    for src in GEMM_SOURCES:
+        obj = os.path.join(BUILD_DIR, src + ".o")
+        jobs.append(["g++", *HOST_FLAGS, "-D__HIP_PLATFORM_AMD__", "-isystem",
+                     os.path.join(ROCM, "include"), *incs, "-c", os.path.join(CSRC, src), "-o", obj])
     for src in HIP_SOURCES + PROBE_SOURCES:
         obj = os.path.join(BUILD_DIR, src + ".o")
         jobs.append([_hipcc(), *HIP_FLAGS, *incs, "-c", os.path.join(CSRC, src), "-o", obj])
@@ -77,13 +86,18 @@ def build(verbose: bool = False) -> str:
         list(ex.map(lambda c: _run(c, verbose), jobs))
     objs = [j[-1] for j in jobs if j[-1] not in stamp_objs]
     probe_objs = [o for o in objs if os.path.basename(o)[:-2] in PROBE_SOURCES]
-    lib_objs = [o for o in objs if o not in probe_objs]
+    gemm_objs = [o for o in objs if os.path.basename(o)[:-2] in GEMM_SOURCES]
+    lib_objs = [o for o in objs if o not in probe_objs and o not in gemm_objs]
     host_objs = [o for o in lib_objs if os.path.basename(o)[:-2] in HOST_SOURCES]
     for path, ob in ((LIB_PATH, lib_objs), (PROBE_LIB_PATH, probe_objs),
                      (STAMPS_LIB_PATH, host_objs + stamp_objs)):
         tmp = path + ".tmp"
         _run([_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *ob, "-o", tmp], verbose)
         shutil.move(tmp, path)
+    rocm_lib = os.path.join(ROCM, "lib")
+    _run(["g++", "-shared", "-fPIC", *gemm_objs, "-L", rocm_lib, "-lhipblaslt", "-lamdhip64",
+          f"-Wl,-rpath,{rocm_lib}", "-o", GEMM_LIB_PATH + ".tmp"], verbose)
+    shutil.move(GEMM_LIB_PATH + ".tmp", GEMM_LIB_PATH)
     return LIB_PATH
 
 

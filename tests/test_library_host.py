@@ -75,6 +75,38 @@ def test_probe_library_exports_its_header(lib):
     assert x(addr, 8, 96, None) == 1                             # bad thread count
 
 
+def test_gemm_ref_library_exports_its_header(lib):
+    """libfqgemm.so (the hipBLASLt bf16 GEMM comparator) exports what
+    include/fq_gemm_ref.h declares, and rejects bad arguments on the host
+    before any HIP or hipBLASLt call."""
+    from paper_2608_15531_amd import gemm_ref
+    with open(os.path.join(ROOT, "include", "fq_gemm_ref.h")) as f:
+        header = f.read()
+    declared = set(re.findall(r"^\s*(?:int|const char\*)\s+(fq_\w+)\(", header, re.M))
+    assert declared == set(gemm_ref.EXPORTS)
+    for name, value in (("FQ_REF_W_KN", gemm_ref.W_KN), ("FQ_REF_W_NK", gemm_ref.W_NK),
+                        ("FQ_REF_HEURISTIC", gemm_ref.HEURISTIC),
+                        ("FQ_REF_EXHAUSTIVE", gemm_ref.EXHAUSTIVE)):
+        assert re.search(rf"#define {name} {value}\b", header)
+    glib = gemm_ref.load()
+    for name in declared:
+        assert getattr(glib, name) is not None
+    n = C.c_int32(-1)
+    prep = glib.fq_ref_gemm_bf16_prepare
+    assert prep(0, 64, 64, 0, 0, 4, 0, C.byref(n)) == 1              # M = 0
+    assert prep(1, 64, 64, 2, 0, 4, 0, C.byref(n)) == 1              # unknown layout
+    assert prep(1, 64, 64, 0, 2, 4, 0, C.byref(n)) == 1              # unknown source
+    assert prep(1, 64, 64, 0, 0, 0, 0, C.byref(n)) == 1              # no candidates asked
+    assert prep(1, 64, 64, 0, 0, 4097, 0, C.byref(n)) == 1           # too many asked
+    assert prep(1, 64, 1 << 21, 0, 0, 4, 0, C.byref(n)) == 1         # N beyond 2^20
+    assert prep(1, 64, 64, 0, 0, 4, 0, None) == 1                    # no output
+    assert glib.fq_ref_gemm_last_error() == b"n_candidates is NULL"
+    assert n.value == -1
+    assert glib.fq_ref_gemm_bf16_candidate(1, 64, 64, 3, 0, None, None, 0) == 1
+    assert glib.fq_ref_gemm_bf16(None, None, None, 1, 64, 64, 0, 0, None, 0, None) == 1
+    assert b"device pointers" in glib.fq_ref_gemm_last_error()
+
+
 def test_instrumented_build_exports(lib):
     """libfq_stamps.so, the build with per-wave timestamps, exports every entry
     point of include/fq.h and what include/fq_debug.h declares, and rejects
