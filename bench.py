@@ -1247,6 +1247,39 @@ def launch_timeline(torch, dev, R: int = 8):
     print("\n".join(out))
 
 
+def gemm_search_check(torch, dev, R: int = 8):
+    """Markdown on stdout: for each decode shape at M = 1 and 16, the bf16
+    GEMM comparator's fastest candidate from hipBLASLt's heuristic (the
+    search bench.py uses) against the fastest of every algorithm the library
+    holds that accepts the problem (both weight layouts each time)."""
+    from paper_2608_15531_amd import gemm_ref
+    out = ["# bf16 GEMM comparator: heuristic search against exhaustive search", "",
+           "Command (repo root, MI355X, ROCm 7.2):", "",
+           "    python3 -u bench.py --gemm-search-check", "",
+           f"Each candidate: a graph of calls cycling over rotated bf16 weight copies (as in "
+           f"bench.py's comparison), the fastest re-timed; heuristic: up to {GEMM_CANDIDATES} "
+           "candidates per layout.  `first` is hipBLASLt's own first heuristic choice in the "
+           "[K][N] layout.", "",
+           "| matmul | search | candidates | best us | layout | best kernel (tile) | first us |",
+           "|---|---|---|---|---|---|---|"]
+    for name, K, N in SHAPES:
+        copies = max(2, min(R, int(2.2e9 // (2 * K * N))))
+        for M in (1, 16):
+            for label, src, mc in (("heuristic", gemm_ref.HEURISTIC, GEMM_CANDIDATES),
+                                   ("exhaustive", gemm_ref.EXHAUSTIVE, 4096)):
+                comp = GemmComparator(torch, dev, source=src, max_candidates=mc)
+                Ws = comp.weights(K, N, copies)
+                b = comp.search(M, K, N, Ws, 40)
+                tile = b["kernel"].split("_MT")[1].split("_")[0] if "_MT" in b["kernel"] else "?"
+                first = f"{b['heuristic_first_us']:.3f}" if src == gemm_ref.HEURISTIC else "-"
+                out.append(f"| {name}/M{M} | {label} | {b['candidates']} | {b['us']:.3f} | "
+                           f"{b['layout']} | MT{tile} | {first} |")
+                log(out[-1])
+                del Ws, comp
+                torch.cuda.empty_cache()
+    print("\n".join(out))
+
+
 def xcd_probe(torch, dev):
     """Markdown on stdout: the XCD each workgroup runs on, against workgroup
     index mod 8 (the placement the matmul kernels' workgroup dealing assumes
@@ -1288,15 +1321,17 @@ def trace_pass(fq, torch, order, launch, R, dev):
     comp = GemmComparator(torch, dev)
     gemm, operands = [], []
     for name, K, N in SHAPES:
-        Ws = comp.weights(K, N, 2)
+        # rotated weight copies as in the timed comparison, so that no call
+        # finds its weight in the last-level cache; made now, so that only
+        # the comparator's kernels run after the fused cases
+        Ws = comp.weights(K, N, max(2, min(R, int(2.2e9 // (2 * K * N)))))
         for M in (1, 16):
             best = comp.search(M, K, N, Ws, 2)
             gemm.append({"case": f"{name}/M{M}", "M": M, "K": K, "N": N, "layout": best["layout"],
-                         "kernel": best["kernel"], "index": best["index"],
+                         "kernel": best["kernel"], "index": best["index"], "copies": len(Ws),
                          "bytes": 2 * K * N + 2 * M * K + 2 * M * N})
-            # operands made now, so that only the comparator's kernels run
-            # after the fused cases
-            operands.append((Ws[0].view((K, N) if best["layout"] == "kn" else (N, K)),
+            shape = (K, N) if best["layout"] == "kn" else (N, K)
+            operands.append(([W.view(shape) for W in Ws],
                              torch.randn(M, K, device=dev, dtype=torch.bfloat16),
                              torch.empty(M, N, device=dev, dtype=torch.bfloat16)))
         del Ws
@@ -1312,10 +1347,10 @@ def trace_pass(fq, torch, order, launch, R, dev):
                     "bytes": c.bytes, "launches": L * (1 + TRACE_WARM + TRACE_REPS),
                     "untimed": L * (1 + TRACE_WARM)})
         del g
-    for e, (W, x, y) in zip(gemm, operands):
+    for e, (Ws, x, y) in zip(gemm, operands):
         # each (M, K, N) was prepared once, by its search: the index still holds
-        for _ in range(GEMM_TRACE_CALLS):
-            comp.g.gemm(x, W, y, e["layout"], e["index"], comp.ws)
+        for i in range(GEMM_TRACE_CALLS):
+            comp.g.gemm(x, Ws[i % len(Ws)], y, e["layout"], e["index"], comp.ws)
         torch.cuda.synchronize()
     del operands
     # prelude: main() launches every case once eagerly before this pass
@@ -1394,10 +1429,11 @@ def trace_per_matmul(trace_csv, log_path):
     calls = meta["gemm_calls"]
     out += ["", "bf16 GEMM comparator: hipBLASLt through libfqgemm (include/fq_gemm_ref.h), the "
                 "candidate its search kept (fastest of the heuristic candidates in the [K][N] and "
-                f"[N][K] weight layouts), {calls} eager calls per case after the fused matmuls; "
-                "kernel-only durations from the same trace.  Bytes: bf16 W, X and Y.", "",
-            "| matmul | layout | kernel | calls | median us | other dispatches | bytes | "
-            "GB/s (median) |", "|---|---|---|---|---|---|---|---|"]
+                f"[N][K] weight layouts), {calls} eager calls per case after the fused matmuls, "
+                "cycling over rotated weight copies like the fused cases; kernel-only durations "
+                "from the same trace.  Bytes: bf16 W, X and Y.", "",
+            "| matmul | layout | kernel | calls | weight copies | median us | other dispatches | "
+            "bytes | GB/s (median) |", "|---|---|---|---|---|---|---|---|---|"]
     j = 0
     for e in meta["gemm"]:
         own, others = [], 0
@@ -1413,7 +1449,7 @@ def trace_per_matmul(trace_csv, log_path):
                              f"expected {calls}")
         med = float(np.median(own)) / 1e3
         out.append(f"| {e['case']} | {e['layout']} | `{e['kernel'][:110]}` | {calls} | "
-                   f"{med:.3f} | {others} | {e['bytes']} | {e['bytes'] / med / 1e3:.0f} |")
+                   f"{e['copies']} | {med:.3f} | {others} | {e['bytes']} | {e['bytes'] / med / 1e3:.0f} |")
     print("\n".join(out))
 
 
@@ -1456,6 +1492,9 @@ def main():
                     help="markdown: cost of each kind of per-tile load (fq_probe_tile_loads)")
     ap.add_argument("--launch-timeline", action="store_true",
                     help="markdown: per-wave launch timeline from the instrumented build")
+    ap.add_argument("--gemm-search-check", action="store_true",
+                    help="markdown: the bf16 GEMM comparator's heuristic search against an "
+                         "exhaustive one over every supported hipBLASLt algorithm")
     ap.add_argument("--xcd-probe", action="store_true",
                     help="markdown: the XCD each workgroup runs on, for the grid sizes the "
                          "kernels use")
@@ -1556,6 +1595,9 @@ def main():
         return
     if args.xcd_probe:
         xcd_probe(torch, dev)
+        return
+    if args.gemm_search_check:
+        gemm_search_check(torch, dev)
         return
     if args.tile_load_probe:
         tile_load_probe(torch, dev)
