@@ -22,8 +22,11 @@
  * returns 0 on success, 1 for an invalid argument, 2 when the problem has not
  * been prepared or the candidate index is out of range, and 3 when a HIP or
  * hipBLASLt call failed; fq_ref_gemm_last_error() then gives the reason.
- * The functions may be called from several host threads; calls that share a
- * problem see the candidate list of the last prepare.
+ * One hipBLASLt handle per device lives until the process ends.  The
+ * library's own tables are guarded by a mutex, but calls that enqueue work
+ * share that handle: the caller serialises fq_ref_gemm_bf16 calls made from
+ * several host threads.  Calls that share a problem see the candidate list
+ * of the last prepare.
  */
 #ifndef FQ_GEMM_REF_H
 #define FQ_GEMM_REF_H
@@ -83,8 +86,8 @@ int fq_ref_gemm_bf16_candidate(int32_t M, int32_t K, int32_t N, int32_t layout,
  *   Y          device, bf16 row-major [M][N], overwritten;
  *   workspace  device buffer of workspace_bytes bytes, at least what the
  *              candidate needs (NULL allowed when it needs none).
- * The buffers belong to the caller and must not overlap Y.  Launches only
- * hipBLASLt's kernels; no memory is allocated.
+ * The buffers belong to the caller and must not overlap Y.  The library
+ * allocates nothing itself; the work is hipBLASLt's kernels.
  */
 int fq_ref_gemm_bf16(const void* X, const void* W, void* Y, int32_t M, int32_t K, int32_t N,
                      int32_t layout, int32_t candidate, void* workspace,
