@@ -1187,6 +1187,61 @@ def tile_load_probe(torch, dev, R: int = 4):
     print("\n".join(out))
 
 
+STRIP_PROBE_CONFIGS = {   # (strip columns, waves, split) per shape; the plan's own is added
+    "qkv": [(64, 4, 1), (64, 8, 2), (32, 8, 1), (32, 4, 2), (16, 8, 1), (16, 4, 1)],
+    "o": [(64, 4, 4), (64, 8, 2), (32, 8, 1), (32, 4, 2), (16, 8, 1), (16, 4, 1)],
+    "gate_up": [(64, 4, 1), (64, 8, 1), (32, 8, 1), (32, 4, 1), (16, 8, 1)],
+    "down": [(64, 4, 8), (64, 8, 4), (32, 8, 2), (32, 4, 4), (16, 8, 1), (16, 4, 2)],
+}
+
+
+def strip_load_probe(fq, torch, dev, R: int = 8):
+    """Markdown on stdout: the fused kernel's per-tile loads without its
+    compute (fq_probe_strip_loads) for several strip widths, splits and wave
+    counts on each decode shape, graph replays over R rotated buffers; the
+    launch shape the library plans at M = 1 is marked."""
+    from paper_2608_15531_amd import probe
+    out = ["# Launch shapes by their loads alone: strip width, split and waves", "",
+           "Command (repo root, MI355X, ROCm 7.2):", "",
+           "    python3 -u bench.py --strip-load-probe > profiles/strip_load_probe.md", "",
+           "`fq_probe_strip_loads` (include/fq_probe.h) issues the fused kernel's per-tile loads "
+           "(four code loads of strip/4 bytes, one 16-byte X load and one 16-byte Tile-COO group "
+           f"load per lane and tile, {TILE_PROBE_GPT} groups per tile; two tiles in flight per "
+           "wave) and nothing else, for one (strip width, waves, split) launch shape at a time.  "
+           f"Graph replays over {R} rotated buffers; us per launch.  `plan` marks the shape the "
+           "library launches at M = 1 (its cross-workgroup reduction, when split > 1, is not "
+           "part of the probe).", "",
+           "| matmul | strip columns | waves | split | workgroups | us per launch | plan |",
+           "|---|---|---|---|---|---|---|"]
+    for name, K, N in SHAPES:
+        T = K // 128
+        cfg = fq.fq_launch_config(1, K, N)
+        plan = (cfg["strip_cols"], cfg["dense_waves"], cfg["split_k"])
+        shapes = list(STRIP_PROBE_CONFIGS[name])
+        if plan not in shapes:
+            shapes.insert(0, plan)
+        codes = [torch.zeros(K * N // 8, dtype=torch.int32, device=dev) for _ in range(R)]
+        groups = [torch.zeros(T * (N // 64) * TILE_PROBE_GPT * 4, dtype=torch.int32, device=dev)
+                  for _ in range(R)]
+        x = torch.zeros(K, dtype=torch.int16, device=dev)
+        sink = torch.zeros(N, dtype=torch.int32, device=dev)
+        for sc, nw, S in shapes:
+            if T // S < nw or N // sc * S > N:
+                continue
+            L = 4 * R
+            g = capture_graph(torch, lambda: [probe.fq_probe_strip_loads(
+                codes[i % R], x, groups[i % R], K, N, sc, nw, S, TILE_PROBE_GPT, sink)
+                for i in range(L)])
+            us = min(graph_us(torch, g, L, 10), graph_us(torch, g, L, 10))
+            del g
+            out.append(f"| {name} | {sc} | {nw} | {S} | {N // sc * S} | {us:.2f} | "
+                       f"{'yes' if (sc, nw, S) == plan else ''} |")
+            log(out[-1])
+        del codes, groups
+        torch.cuda.empty_cache()
+    print("\n".join(out))
+
+
 def launch_timeline(torch, dev, R: int = 8):
     """Markdown on stdout: where a fused launch's time goes, per wave, from the
     instrumented build (libfq_stamps.so): each Llama-3-8B decode matmul in a
@@ -1492,6 +1547,9 @@ def main():
                     help="markdown: cost of each kind of per-tile load (fq_probe_tile_loads)")
     ap.add_argument("--launch-timeline", action="store_true",
                     help="markdown: per-wave launch timeline from the instrumented build")
+    ap.add_argument("--strip-load-probe", action="store_true",
+                    help="markdown: launch shapes (strip width, waves, split) compared by "
+                         "the fused kernel's per-tile loads alone")
     ap.add_argument("--gemm-search-check", action="store_true",
                     help="markdown: the bf16 GEMM comparator's heuristic search against an "
                          "exhaustive one over every supported hipBLASLt algorithm")
@@ -1598,6 +1656,9 @@ def main():
         return
     if args.gemm_search_check:
         gemm_search_check(torch, dev)
+        return
+    if args.strip_load_probe:
+        strip_load_probe(fq, torch, dev)
         return
     if args.tile_load_probe:
         tile_load_probe(torch, dev)

@@ -92,6 +92,29 @@ int fq_probe_tile_loads(const void* codes, const void* scales, const void* zeros
                         const void* groups, int32_t K, int32_t N, int32_t groups_per_tile,
                         uint32_t extra, uint32_t* sink, void* stream);
 
+/*
+ * fq_probe_strip_loads -- enqueue one kernel that issues the per-tile loads
+ * of the fused matmul for a chosen strip width, split and wave count, without
+ * its compute, to compare launch shapes by their loads alone.  Workgroup =
+ * (strip, one of `split` contiguous K ranges), `waves` waves splitting that
+ * range, two 128-row tiles in flight per wave.  Per tile and lane: four code
+ * loads of strip_cols / 4 bytes (the lane's strip_cols / 16 columns of four
+ * packed rows), one 16-byte X load and one 16-byte Tile-COO group load.
+ *   codes, x, groups  as for fq_probe_tile_loads
+ *   strip_cols        16, 32 or 64
+ *   waves             4 or 8
+ *   split             >= 1, with (K/128) / split >= waves; (N / strip_cols) *
+ *                     split <= 65536 workgroups
+ *   groups_per_tile   1..64
+ *   sink              device uint32 [(N / strip_cols) * split]; contents
+ *                     unspecified after the call
+ * Returns 0 on success, 1 on a bad argument (nothing launched), 2 when the
+ * HIP runtime reported a launch error.
+ */
+int fq_probe_strip_loads(const void* codes, const void* x, const void* groups, int32_t K,
+                         int32_t N, int32_t strip_cols, int32_t waves, int32_t split,
+                         int32_t groups_per_tile, uint32_t* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

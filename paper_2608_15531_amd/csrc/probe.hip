@@ -121,6 +121,75 @@ int launch_tiles(const void* c, const void* s, const void* z, const void* x, con
   return hipGetLastError() == hipSuccess ? 0 : 2;
 }
 
+// The per-tile loads of the fused kernel for a given strip width, split and
+// wave count, without its compute: workgroup = (strip, K range), XCD-aware
+// order, NW waves splitting the range into contiguous tiles, two tiles in
+// flight per wave.  Per tile and lane: four code loads (SC / 4 bytes each,
+// one per 32-row step: the lane's SC / 16 columns of four packed rows), one
+// 16-byte X load and one 16-byte Tile-COO group load of the 64-column tile
+// the strip lies in.  Scales and zero-points are left out: the kernel loads
+// them once per wave.
+template <int SC> struct StripWords;
+template <> struct StripWords<16> { typedef uint32_t type; };
+template <> struct StripWords<32> { typedef uint2 type; };
+template <> struct StripWords<64> { typedef uint4 type; };
+
+__device__ __forceinline__ uint32_t fold_words(uint32_t v) { return v; }
+__device__ __forceinline__ uint32_t fold_words(uint2 v) { return v.x ^ v.y; }
+__device__ __forceinline__ uint32_t fold_words(uint4 v) { return v.x ^ v.y ^ v.z ^ v.w; }
+
+template <int SC, int NW>
+__global__ void __launch_bounds__(64 * NW) strip_loads(const uint32_t* __restrict__ codes,
+                                                       const uint4* __restrict__ x,
+                                                       const uint4* __restrict__ groups, int T,
+                                                       int N, int S, int gpt, uint32_t* sink) {
+  typedef typename StripWords<SC>::type W;
+  const int G = gridDim.x, b = blockIdx.x;
+  const int u = (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+  const int strip = u / S, part = u % S;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 4, c4 = lane & 15;
+  const int p_lo = T * part / S, p_hi = T * (part + 1) / S, pt = p_hi - p_lo;
+  const int t_lo = p_lo + pt * wave / NW, t_hi = p_lo + pt * (wave + 1) / NW;
+  const int col = strip * SC + (SC / 16) * c4;
+  const size_t tile64 = size_t(strip * SC / 64);
+  uint32_t acc = 0;
+  W w[2][4];
+  uint4 xv[2], gv[2];
+  auto issue = [&](int t, int i) {
+    t = t < t_hi ? t : t_hi - 1;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+      w[i][st] = *reinterpret_cast<const W*>(codes + (size_t(t) * 16 + 4 * st + h) * N + col);
+    xv[i] = x[size_t(t) * 16 + c4];
+    gv[i] = groups[(tile64 * T + t) * gpt + min(lane, gpt - 1)];
+  };
+  if (t_lo < t_hi) {
+    issue(t_lo, 0);
+    issue(t_lo + 1, 1);
+    for (int t = t_lo; t < t_hi; t += 2) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        if (i == 0 || t + i < t_hi) {
+#pragma unroll
+          for (int st = 0; st < 4; ++st) acc ^= fold_words(w[i][st]);
+          acc ^= xv[i].x ^ xv[i].w ^ gv[i].x ^ gv[i].w;
+        }
+        issue(t + i + 2, i);
+      }
+    }
+  }
+  if (acc == kNeverStored) sink[b] = acc;
+}
+
+template <int SC, int NW>
+int launch_strips(const void* c, const void* x, const void* g, int T, int N, int S, int gpt,
+                  uint32_t* sink, hipStream_t st) {
+  hipLaunchKernelGGL((strip_loads<SC, NW>), dim3(unsigned(N / SC * S)), dim3(64 * NW), 0, st,
+                     static_cast<const uint32_t*>(c), static_cast<const uint4*>(x),
+                     static_cast<const uint4*>(g), T, N, S, gpt, sink);
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
+
 }  // namespace
 
 extern "C" int fq_probe_tile_loads(const void* codes, const void* scales, const void* zeros,
@@ -182,5 +251,33 @@ extern "C" int fq_probe_stream_read(const void* src, size_t bytes, int32_t workg
     case 4: return launch<4>(src, n16, workgroups, waves, sink, s);
     case 8: return launch<8>(src, n16, workgroups, waves, sink, s);
     default: return 1;
+  }
+}
+
+extern "C" int fq_probe_strip_loads(const void* codes, const void* x, const void* groups,
+                                    int32_t K, int32_t N, int32_t strip_cols, int32_t waves,
+                                    int32_t split, int32_t groups_per_tile, uint32_t* sink,
+                                    void* stream) {
+  if (!codes || !x || !groups || !sink) return 1;
+  if (K < 128 || K % 128 || N < 64 || N % 64) return 1;
+  if (strip_cols != 16 && strip_cols != 32 && strip_cols != 64) return 1;
+  if (waves != 4 && waves != 8) return 1;
+  const int T = K / 128;
+  if (split < 1 || T / split < waves) return 1;   // every wave has a tile
+  if (int64_t(N / strip_cols) * split > 65536) return 1;
+  if (groups_per_tile < 1 || groups_per_tile > 64) return 1;
+  if ((reinterpret_cast<uintptr_t>(codes) | reinterpret_cast<uintptr_t>(x) |
+       reinterpret_cast<uintptr_t>(groups)) & 15)
+    return 1;
+  if (reinterpret_cast<uintptr_t>(sink) & 3) return 1;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int gpt = groups_per_tile;
+  switch (strip_cols * 16 + waves) {
+    case 16 * 16 + 4: return launch_strips<16, 4>(codes, x, groups, T, N, split, gpt, sink, s);
+    case 16 * 16 + 8: return launch_strips<16, 8>(codes, x, groups, T, N, split, gpt, sink, s);
+    case 32 * 16 + 4: return launch_strips<32, 4>(codes, x, groups, T, N, split, gpt, sink, s);
+    case 32 * 16 + 8: return launch_strips<32, 8>(codes, x, groups, T, N, split, gpt, sink, s);
+    case 64 * 16 + 4: return launch_strips<64, 4>(codes, x, groups, T, N, split, gpt, sink, s);
+    default: return launch_strips<64, 8>(codes, x, groups, T, N, split, gpt, sink, s);
   }
 }

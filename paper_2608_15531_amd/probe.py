@@ -10,7 +10,8 @@ import threading
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 PROBE_LIB_PATH = os.path.join(_HERE, "libfqprobe.so")
-EXPORTS = ("fq_probe_stream_read", "fq_probe_workgroup_xcd", "fq_probe_tile_loads")
+EXPORTS = ("fq_probe_stream_read", "fq_probe_workgroup_xcd", "fq_probe_tile_loads",
+           "fq_probe_strip_loads")
 FQ_PROBE_SCALES, FQ_PROBE_ZEROS, FQ_PROBE_X, FQ_PROBE_GROUPS, FQ_PROBE_MASKED = 1, 2, 4, 8, 16
 
 _lib = None
@@ -33,6 +34,9 @@ def load() -> C.CDLL:
             lib.fq_probe_tile_loads.argtypes = [C.c_void_p] * 5 + [C.c_int32, C.c_int32, C.c_int32,
                                                                    C.c_uint32, C.c_void_p, C.c_void_p]
             lib.fq_probe_tile_loads.restype = C.c_int
+            lib.fq_probe_strip_loads.argtypes = [C.c_void_p] * 3 + [C.c_int32] * 6 + [
+                C.c_void_p, C.c_void_p]
+            lib.fq_probe_strip_loads.restype = C.c_int
             _lib = lib
     return _lib
 
@@ -83,3 +87,24 @@ def fq_probe_tile_loads(codes, scales, zeros, x, groups, K: int, N: int, groups_
                                     extra, sink.data_ptr(), int(stream.cuda_stream))
     if rc != 0:
         raise RuntimeError(f"fq_probe_tile_loads failed ({rc})")
+
+
+def fq_probe_strip_loads(codes, x, groups, K: int, N: int, strip_cols: int, waves: int,
+                         split: int, groups_per_tile: int, sink, stream=None) -> None:
+    """Enqueue the strip-width load probe (see include/fq_probe.h) on device
+    tensors; sink: device tensor of at least (N / strip_cols) * split int32
+    words."""
+    import torch
+    T = K // 128
+    if (codes.numel() * codes.element_size() < K * N // 2
+            or x.numel() * x.element_size() < 2 * K
+            or groups.numel() * groups.element_size() < 16 * groups_per_tile * T * (N // 64)
+            or sink.numel() * sink.element_size() < 4 * (N // max(1, strip_cols)) * split):
+        raise ValueError("fq_probe_strip_loads: buffer too small")
+    if stream is None:
+        stream = torch.cuda.current_stream(codes.device)
+    rc = load().fq_probe_strip_loads(codes.data_ptr(), x.data_ptr(), groups.data_ptr(), K, N,
+                                     strip_cols, waves, split, groups_per_tile, sink.data_ptr(),
+                                     int(stream.cuda_stream))
+    if rc != 0:
+        raise RuntimeError(f"fq_probe_strip_loads failed ({rc})")

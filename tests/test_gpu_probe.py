@@ -45,6 +45,21 @@ def test_tile_loads_runs(gpu_lib, extra):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("cols,waves,split", [(16, 8, 1), (16, 4, 2), (32, 8, 1), (32, 4, 2),
+                                              (64, 4, 2), (64, 8, 1)])
+def test_strip_loads_runs(gpu_lib, cols, waves, split):
+    from paper_2608_15531_amd import probe
+    K, N, gpt = 1024, 512, 21
+    T = K // 128
+    dev = "cuda"
+    codes = torch.ones(K * N // 8, dtype=torch.int32, device=dev)
+    x = torch.ones(K, dtype=torch.int16, device=dev)
+    groups = torch.ones(T * (N // 64) * gpt * 4, dtype=torch.int32, device=dev)
+    sink = torch.zeros(N // cols * split, dtype=torch.int32, device=dev)
+    probe.fq_probe_strip_loads(codes, x, groups, K, N, cols, waves, split, gpt, sink)
+    torch.cuda.synchronize()
+
+
 def test_instrumented_build_stamps_and_results(gpu_lib):
     """The same fused launch through libfq.so and through libfq_stamps.so: the
     results agree to the f32 tolerance, and every wave's four stamps are in

@@ -68,6 +68,17 @@ def test_probe_library_exports_its_header(lib):
     assert t(addr, addr, addr, addr, addr, 128, 64, 21, 32, addr, None) == 1     # no such load
     assert t(addr, addr, addr, addr, addr, 128, 64, 21, 1, addr, None) == 1      # scales alone
     assert t(addr + 8, addr, addr, addr, addr, 128, 64, 21, 0, addr, None) == 1  # codes misaligned
+    sl = plib.fq_probe_strip_loads
+    assert sl(None, addr, addr, 1024, 512, 32, 8, 1, 21, addr, None) == 1      # null codes
+    assert sl(addr, addr, addr, 1000, 512, 32, 8, 1, 21, addr, None) == 1      # K % 128
+    assert sl(addr, addr, addr, 1024, 96, 32, 8, 1, 21, addr, None) == 1       # N % 64
+    assert sl(addr, addr, addr, 1024, 512, 48, 8, 1, 21, addr, None) == 1      # strip width
+    assert sl(addr, addr, addr, 1024, 512, 32, 2, 1, 21, addr, None) == 1      # wave count
+    assert sl(addr, addr, addr, 1024, 512, 32, 8, 0, 21, addr, None) == 1      # no split
+    assert sl(addr, addr, addr, 1024, 512, 32, 8, 2, 21, addr, None) == 1      # 4 tiles < 8 waves
+    assert sl(addr, addr, addr, 1024, 512, 32, 4, 1, 65, addr, None) == 1      # > 64 groups
+    assert sl(addr + 8, addr, addr, 1024, 512, 32, 4, 1, 21, addr, None) == 1  # codes misaligned
+    assert sl(addr, addr, addr, 1024, 512, 32, 4, 1, 21, addr + 2, None) == 1  # sink misaligned
     x = plib.fq_probe_workgroup_xcd
     assert x(None, 8, 64, None) == 1                             # null output
     assert x(addr + 2, 8, 64, None) == 1                         # misaligned output
