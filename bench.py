@@ -742,6 +742,13 @@ def ablation_summary(log_path):
     print("\n".join(out))
 
 
+def _gemm_cols(r):
+    """The bf16 GEMM comparator's two table cells of a sweep record."""
+    if "bf16_gemm_us" not in r:
+        return "- | -"
+    return f"{r['bf16_gemm_us']:.2f} ({r['bf16_gemm_layout']}) | {r['speedup_vs_bf16_gemm']:.2f}x"
+
+
 def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
     """Markdown summary of the three sweeps and the MFMA counter pass
     (stdout).  No GPU."""
@@ -768,7 +775,10 @@ def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
            "(larger M): `alg TF` = (2MKN + 2M nnz) / t, `MFMA TF` = FLOPs the matrix cores "
            "execute (dense, row-sum and outlier-image MFMAs, padded rows included) / t, against "
            "the 2500 TFLOP/s dense bf16 peak.  Tile-COO: the library default packing (by-bucket "
-           "groups, one bucket per tile).", "",
+           "groups, one bucket per tile).  `bf16 GEMM us` (70B and larger M): the bf16 GEMM "
+           "comparator on a dense bf16 weight of the same K x N (hipBLASLt through libfqgemm, "
+           "fastest of its heuristic candidates in both weight layouts, over rotated bf16 "
+           "copies); `fused vs bf16 GEMM` = its time / the fused time.", "",
            "## Density and structure (M=8, 4096x14336)", "",
            "| outliers | clustered share | Tile-COO MB | fused us | GB/s | % peak | unfused us | "
            "fused vs unfused | dense-only us | kernel |", "|---|---|---|---|---|---|---|---|---|---|"]
@@ -779,11 +789,12 @@ def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
                    f"{r['dense_only_us']:.2f} | `{r['kernel']}` |")
     out += ["", "## Llama-3-70B decode linears (1% uniform)", "",
             "| K x N | M | fused us | GB/s | % peak | unfused us | fused vs unfused | "
-            "dense-only us | kernel |", "|---|---|---|---|---|---|---|---|---|"]
+            "dense-only us | bf16 GEMM us | fused vs bf16 GEMM | kernel |",
+            "|---|---|---|---|---|---|---|---|---|---|---|"]
     for r in sw["70b"]:
         out.append(f"| {r['K']}x{r['N']} | {r['M']} | {r['fused_us']:.2f} | {r['fused_GBs']:.0f} | "
                    f"{r['pct_hbm_peak']} | {r['unfused_us']:.2f} | {r['fused_vs_unfused']:.2f}x | "
-                   f"{r['dense_only_us']:.2f} | `{r['kernel']}` |")
+                   f"{r['dense_only_us']:.2f} | {_gemm_cols(r)} | `{r['kernel']}` |")
     out += ["", "Layer aggregate (the four Llama-3-70B linears of one decode layer: total "
                 "algorithmic bytes / total fused time):", "",
             "| M | bytes | fused us | GB/s | % peak | unfused us | fused vs unfused |",
@@ -797,13 +808,13 @@ def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
                    f"{100 * b / t / 1e3 / HBM_PEAK_GBS:.1f} | {tu:.2f} | {tu / t:.2f}x |")
     out += ["", "## Larger M (1% uniform)", "",
             "| K x N | M | fused us | GB/s | % peak | alg TF | MFMA TF | MFMA % peak | unfused us "
-            "| fused vs unfused | dense-only us | kernel |",
-            "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+            "| fused vs unfused | dense-only us | bf16 GEMM us | fused vs bf16 GEMM | kernel |",
+            "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for r in sw["large-m"]:
         out.append(f"| {r['K']}x{r['N']} | {r['M']} | {r['fused_us']:.2f} | {r['fused_GBs']:.0f} | "
                    f"{r['pct_hbm_peak']} | {r['alg_TFLOPs']} | {r['mfma_TFLOPs']} | "
                    f"{r['mfma_util_pct']} | {r['unfused_us']:.2f} | {r['fused_vs_unfused']:.2f}x | "
-                   f"{r['dense_only_us']:.2f} | `{r['kernel']}` |")
+                   f"{r['dense_only_us']:.2f} | {_gemm_cols(r)} | `{r['kernel']}` |")
     out += ["", "## MFMA counters (larger M)", "",
             "Four eager launches per case.  `MfmaUtil` is rocprofv3's derived metric (MFMA busy "
             "cycles summed over SIMDs / (GPU-active cycles x SIMDs)); `MfmaFlopsBF16` counts 512 "
@@ -858,6 +869,10 @@ def sweep(fq, torch, which, dev, copies_min=4):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / (reps * L)
 
+    # the bf16 GEMM comparator beside the 70B and larger-M matmuls (the
+    # paper's batch-size comparison with a vendor bf16 GEMM)
+    comp = GemmComparator(torch, dev) if which in ("70b", "large-m") else None
+
     # weights per (shape, density, structure): enough rotated copies to pass 1 GiB
     weights = {}
     for cfg, si, M, K, N, frac, dist in cases:
@@ -872,6 +887,7 @@ def sweep(fq, torch, which, dev, copies_min=4):
         weights[key] = ([fq.to_device(p, dev)[1:] for _ in range(R)],
                         [fq.TileCOODevice(host, dev) for _ in range(R)], host, p.meta)
         W, T, host, meta = weights[key]
+        Wb = comp.weights(K, N, max(2, min(8, int(2.2e9 // (2 * K * N))))) if comp else None
         mis = {1: 0, 8: 1, 16: 2, 32: 3, 64: 1, 128: 2}
         for c2 in [c for c in cases if (c[3], c[4], c[5], c[6]) == key]:
             M2 = c2[2]
@@ -897,6 +913,11 @@ def sweep(fq, torch, which, dev, copies_min=4):
                    "fused_vs_unfused": round(us_unf / us, 3)}
             if "realised_share" in meta:
                 rec["clustered_share"] = round(meta["realised_share"], 3)
+            if comp is not None:
+                best = comp.search(M2, K, N, Wb, max(2, 160 // len(Wb)))
+                rec.update(bf16_gemm_us=round(best["us"], 3), bf16_gemm_layout=best["layout"],
+                           bf16_gemm_kernel=best["kernel"],
+                           speedup_vs_bf16_gemm=round(best["us"] / us, 3))
             if which == "large-m":
                 alg = 2 * M2 * K * N + 2 * M2 * nnz
                 mf = mfma_flops(fq, M2, K, N)
@@ -904,6 +925,7 @@ def sweep(fq, torch, which, dev, copies_min=4):
                            mfma_TFLOPs=round(mf / us / 1e6, 1),
                            mfma_util_pct=round(100 * mf / us / 1e6 / MFMA_PEAK_TFLOPS, 2))
             print(json.dumps(rec), flush=True)
+        del Wb
 
 
 # Tile-COO packings compared for the element-reordering study (Sec. 3.2.2):
