@@ -166,6 +166,22 @@ class StreamProbe:
         return best
 
 
+def bf16_dequant_weight(torch, Wq, scales, zeros, k, n, v, K, N, group=128):
+    """bf16(dequant(W_Q) + W_O) [K][N] on the device: the dense bf16 weight the
+    bf16 GEMM comparator reads in place of the INT4 codes and the outliers
+    (codes: nibble k % 8 of word [k / 8][n]; zero-points: nibble n % 8 of word
+    [g][n / 8]; outliers: int32 positions, bf16 bits)."""
+    dev = Wq.device
+    sh = torch.arange(0, 32, 4, device=dev, dtype=torch.int32)
+    q = ((Wq.view(K // 8, 1, N) >> sh.view(1, 8, 1)) & 15).view(K // group, group, N)
+    z = ((zeros.view(K // group, N // 8, 1) >> sh.view(1, 1, 8)) & 15).view(K // group, 1, N)
+    w = ((q - z).float() * scales.float().view(K // group, 1, N)).view(K, N)
+    vals = torch.from_numpy(v.view(np.int16).copy()).view(torch.bfloat16).to(dev).float()
+    w.index_put_((torch.from_numpy(k.astype(np.int64)).to(dev),
+                  torch.from_numpy(n.astype(np.int64)).to(dev)), vals, accumulate=True)
+    return w.to(torch.bfloat16)
+
+
 class GemmComparator:
     """The bf16 GEMM comparator (libfqgemm, include/fq_gemm_ref.h): hipBLASLt
     on a dense bf16 weight of the same K x N, fp32 accumulation, bf16 Y.  For
@@ -184,21 +200,34 @@ class GemmComparator:
         self.max_c = max_candidates or GEMM_CANDIDATES
         self.ws = torch.empty(GEMM_WORKSPACE, dtype=torch.uint8, device=dev)
 
-    def weights(self, K, N, copies):
-        return [self.torch.randn(K * N, device=self.dev, dtype=self.torch.bfloat16)
-                for _ in range(copies)]
+    def weights(self, K, N, copies, base=None):
+        """Rotated weight copies per layout, {"kn": [...], "nk": [...]}, as
+        flat bf16 tensors.  base: the [K][N] bf16 weight to copy (its
+        transpose for [N][K]); without it, random values, one set of buffers
+        read in either layout (a GEMM's time does not depend on the values)."""
+        torch = self.torch
+        if base is None:
+            Ws = [torch.randn(K * N, device=self.dev, dtype=torch.bfloat16)
+                  for _ in range(copies)]
+            return {"kn": Ws, "nk": Ws}
+        nk = base.t().contiguous().view(-1)
+        return {"kn": [base.reshape(-1).clone() for _ in range(copies)],
+                "nk": [nk.clone() for _ in range(copies)]}
 
     def _launches(self, x, Ws, y, layout, i):
         K, N = x.shape[1], y.shape[1]
         shape = (K, N) if layout == "kn" else (N, K)
-        return lambda: [self.g.gemm(x, W.view(shape), y, layout, i, self.ws) for W in Ws]
+        return lambda: [self.g.gemm(x, W.view(shape), y, layout, i, self.ws)
+                        for W in Ws[layout]]
 
-    def search(self, M, K, N, Ws, reps):
+    def search(self, M, K, N, Ws, reps, x=None):
         """Times every candidate; returns a dict with the fastest one's
         per-launch us, layout, kernel name and check, the number timed and
-        the us of hipBLASLt's own first choice in the [K][N] layout."""
+        the us of hipBLASLt's own first choice in the [K][N] layout.
+        x: the bf16 activations [M][K] (default: random)."""
         torch, g = self.torch, self.g
-        x = torch.randn(M, K, device=self.dev, dtype=torch.bfloat16)
+        if x is None:
+            x = torch.randn(M, K, device=self.dev, dtype=torch.bfloat16)
         y = torch.empty(M, N, device=self.dev, dtype=torch.bfloat16)
         timed = []
         for layout in self.LAYOUTS:
@@ -215,15 +244,15 @@ class GemmComparator:
                     gr.replay()
                 e1.record()
                 torch.cuda.synchronize()
-                timed.append((e0.elapsed_time(e1) * 1e3 / (4 * len(Ws)), layout, i, name))
+                timed.append((e0.elapsed_time(e1) * 1e3 / (4 * len(Ws[layout])), layout, i, name))
                 del gr
         first = next(t for t in timed if t[1] == "kn" and t[2] == 0)
         _, layout, i, name = min(timed)
         gr = capture_graph(torch, self._launches(x, Ws, y, layout, i))
-        us = graph_us(torch, gr, len(Ws), reps)
+        us = graph_us(torch, gr, len(Ws[layout]), reps)
         del gr
         # the kept candidate computes the product: Y against fp32 torch.matmul
-        W0 = Ws[0].view((K, N) if layout == "kn" else (N, K))
+        W0 = Ws[layout][0].view((K, N) if layout == "kn" else (N, K))
         g.gemm(x, W0, y, layout, i, self.ws)
         ref = x.float() @ (W0.float() if layout == "kn" else W0.float().t())
         # bf16 rounding of Y plus fp32 accumulation in any order
@@ -776,9 +805,9 @@ def sweep_summary(density_log, b70_log, large_m_log, mfma_csv, mfma_log):
            "execute (dense, row-sum and outlier-image MFMAs, padded rows included) / t, against "
            "the 2500 TFLOP/s dense bf16 peak.  Tile-COO: the library default packing (by-bucket "
            "groups, one bucket per tile).  `bf16 GEMM us` (70B and larger M): the bf16 GEMM "
-           "comparator on a dense bf16 weight of the same K x N (hipBLASLt through libfqgemm, "
-           "fastest of its heuristic candidates in both weight layouts, over rotated bf16 "
-           "copies); `fused vs bf16 GEMM` = its time / the fused time.", "",
+           "comparator on bf16(dequant(W_Q) + W_O) and the same X (hipBLASLt through "
+           "libfqgemm, fastest of its heuristic candidates in both weight layouts, over rotated "
+           "bf16 copies); `fused vs bf16 GEMM` = its time / the fused time.", "",
            "## Density and structure (M=8, 4096x14336)", "",
            "| outliers | clustered share | Tile-COO MB | fused us | GB/s | % peak | unfused us | "
            "fused vs unfused | dense-only us | kernel |", "|---|---|---|---|---|---|---|---|---|---|"]
@@ -887,7 +916,9 @@ def sweep(fq, torch, which, dev, copies_min=4):
         weights[key] = ([fq.to_device(p, dev)[1:] for _ in range(R)],
                         [fq.TileCOODevice(host, dev) for _ in range(R)], host, p.meta)
         W, T, host, meta = weights[key]
-        Wb = comp.weights(K, N, max(2, min(8, int(2.2e9 // (2 * K * N))))) if comp else None
+        Wb = comp.weights(K, N, max(2, min(8, int(2.2e9 // (2 * K * N)))),
+                          base=bf16_dequant_weight(torch, *W[0], p.k, p.n, p.v, K, N)) \
+            if comp else None
         mis = {1: 0, 8: 1, 16: 2, 32: 3, 64: 1, 128: 2}
         for c2 in [c for c in cases if (c[3], c[4], c[5], c[6]) == key]:
             M2 = c2[2]
@@ -914,7 +945,7 @@ def sweep(fq, torch, which, dev, copies_min=4):
             if "realised_share" in meta:
                 rec["clustered_share"] = round(meta["realised_share"], 3)
             if comp is not None:
-                best = comp.search(M2, K, N, Wb, max(2, 160 // len(Wb)))
+                best = comp.search(M2, K, N, Wb, max(2, 160 // len(Wb["kn"])), x=x)
                 rec.update(bf16_gemm_us=round(best["us"], 3), bf16_gemm_layout=best["layout"],
                            bf16_gemm_kernel=best["kernel"],
                            speedup_vs_bf16_gemm=round(best["us"] / us, 3))
@@ -1383,7 +1414,7 @@ def xcd_probe(torch, dev):
     print("\n".join(out_lines))
 
 
-TRACE_WARM, TRACE_REPS = 2, 6   # replays per case in the kernel-trace pass
+TRACE_WARM, TRACE_REPS = 2, 7   # replays per case in the kernel-trace pass
 GEMM_TRACE_CALLS = 8            # eager comparator calls per case in that pass
 
 
@@ -1405,10 +1436,11 @@ def trace_pass(fq, torch, order, launch, R, dev):
         for M in (1, 16):
             best = comp.search(M, K, N, Ws, 2)
             gemm.append({"case": f"{name}/M{M}", "M": M, "K": K, "N": N, "layout": best["layout"],
-                         "kernel": best["kernel"], "index": best["index"], "copies": len(Ws),
+                         "kernel": best["kernel"], "index": best["index"],
+                         "copies": len(Ws[best["layout"]]),
                          "bytes": 2 * K * N + 2 * M * K + 2 * M * N})
             shape = (K, N) if best["layout"] == "kn" else (N, K)
-            operands.append(([W.view(shape) for W in Ws],
+            operands.append(([W.view(shape) for W in Ws[best["layout"]]],
                              torch.randn(M, K, device=dev, dtype=torch.bfloat16),
                              torch.empty(M, N, device=dev, dtype=torch.bfloat16)))
         del Ws
@@ -1507,7 +1539,8 @@ def trace_per_matmul(trace_csv, log_path):
     out += ["", "bf16 GEMM comparator: hipBLASLt through libfqgemm (include/fq_gemm_ref.h), the "
                 "candidate its search kept (fastest of the heuristic candidates in the [K][N] and "
                 f"[N][K] weight layouts), {calls} eager calls per case after the fused matmuls, "
-                "cycling over rotated weight copies like the fused cases; kernel-only durations "
+                "cycling over rotated copies of a random bf16 weight of the same shape (a GEMM's "
+                "time does not depend on the values) like the fused cases; kernel-only durations "
                 "from the same trace.  Bytes: bf16 W, X and Y.", "",
             "| matmul | layout | kernel | calls | weight copies | median us | other dispatches | "
             "bytes | GB/s (median) |", "|---|---|---|---|---|---|---|---|---|"]
@@ -1699,6 +1732,7 @@ def main():
     blas = str(torch.backends.cuda.preferred_blas_library())
     cases = []
     pack_s = {}
+    bf16_w = {}   # the bf16 GEMM comparator's weight per shape
     for si, (name, K, N) in enumerate(SHAPES):
         t0 = time.perf_counter()
         p = make_problem(1, K, N, frac=FRAC, seed=seed_for(1, si, 0))
@@ -1711,6 +1745,8 @@ def main():
             weights.append(fq.to_device(p, dev)[1:])
             tcs.append(fq.TileCOODevice(host, dev))
             tcs_p.append(fq.TileCOODevice(host_p, dev))
+        if not args.no_compare:
+            bf16_w[name] = bf16_dequant_weight(torch, *weights[0], p.k, p.n, p.v, K, N)
         log(f"[setup] {name} K={K} N={N}: generate {t1 - t0:.1f}s, pack {pack_s[name]:.2f}s, "
             f"tilecoo {host.sizes.bytes / 1e6:.2f} MB (paper format "
             f"{host_p.sizes.bytes / 1e6:.2f} MB), {R} copies")
@@ -1853,18 +1889,20 @@ def main():
     del probe
 
     if not args.no_compare:
-        # bf16 GEMM comparator: hipBLASLt called directly (libfqgemm), the
-        # fastest of its heuristic candidates in both weight layouts; and
-        # torch.matmul on the same weight for reference.
+        # bf16 GEMM comparator: hipBLASLt called directly (libfqgemm) on
+        # bf16(dequant(W_Q) + W_O) and the same X, the fastest of its
+        # heuristic candidates in both weight layouts; and torch.matmul on the
+        # same operands for reference.
         comp = GemmComparator(torch, dev)
         for si, (name, K, N) in enumerate(SHAPES):
             copies = max(2, min(R, int(2.2e9 // (2 * K * N))))
-            Ws = comp.weights(K, N, copies)
+            Ws = comp.weights(K, N, copies, base=bf16_w.pop(name))
             for d in details:
                 if d["shape"] != name:
                     continue
                 M = d["M"]
-                best = comp.search(M, K, N, Ws, reps)
+                x = next(c for c in order if c.name == name and c.M == M).X
+                best = comp.search(M, K, N, Ws, reps, x=x)
                 gemm_bytes = 2 * K * N + 2 * M * K + 2 * M * N   # bf16 W, X and Y
                 d["bf16_gemm_us"] = round(best["us"], 3)
                 d["bf16_gemm_GBs"] = round(gemm_bytes / best["us"] / 1e3, 1)
@@ -1873,9 +1911,8 @@ def main():
                 d["bf16_gemm_candidates"] = best["candidates"]
                 d["bf16_gemm_heuristic_first_us"] = round(best["heuristic_first_us"], 3)
                 d["speedup_vs_bf16_gemm"] = round(best["us"] / d["fused_us"], 3)
-                x = torch.randn(M, K, device=dev, dtype=torch.bfloat16)
                 out = torch.empty(M, N, device=dev, dtype=torch.bfloat16)
-                g = capture(lambda: [torch.matmul(x, W.view(K, N), out=out) for W in Ws])
+                g = capture(lambda: [torch.matmul(x, W.view(K, N), out=out) for W in Ws["kn"]])
                 d["torch_matmul_us"] = round(graph_us(torch, g, copies, reps), 3)
                 del g
             del Ws
@@ -1943,7 +1980,8 @@ def main():
         },
         "layer_aggregate": layers,
         "tilecoo_paper_format": paper_step,
-        "bf16_gemm_comparator": "hipBLASLt called directly (libfqgemm): bf16 K x N weight, "
+        "bf16_gemm_comparator": "hipBLASLt called directly (libfqgemm): bf16(dequant(W_Q) + "
+                                "W_O) K x N weight and the same X, "
                                 "fp32 accumulation, bf16 Y; fastest of up to "
                                 f"{GEMM_CANDIDATES} heuristic candidates in each of the [K][N] "
                                 "and [N][K] weight layouts; torch_matmul_us: torch.matmul "
