@@ -1467,6 +1467,94 @@ def trace_pass(fq, torch, order, launch, R, dev):
                       "prelude": len(order)}), flush=True)
 
 
+def trace_pass_unfused(fq, torch, order, launch, R):
+    """For a rocprofv3 --kernel-trace run: each (shape, M) case's fused graph
+    and then its unfused graph (4R launches each, TRACE_WARM + TRACE_REPS
+    replays), in step order.  One JSON line names the sequence, so the trace
+    splits per case and variant (--trace-unfused-summary)."""
+    L = 4 * R
+    seq = []
+    for c in order:
+        for variant, per in (("fused", 1), ("unfused", 2)):
+            g = capture_graph(torch, lambda c=c, v=variant: [launch(c, i % R, v) for i in range(L)])
+            for _ in range(TRACE_WARM + TRACE_REPS):
+                g.replay()
+            torch.cuda.synchronize()
+            seq.append({"case": f"{c.name}/M{c.M}", "variant": variant, "per_launch": per,
+                        "dispatches": per * L * (1 + TRACE_WARM + TRACE_REPS),
+                        "untimed": per * L * (1 + TRACE_WARM)})
+            del g
+    print(json.dumps({"trace_pass_unfused": seq, "prelude": len(order)}), flush=True)
+
+
+def trace_unfused_summary(trace_csv, log_path):
+    """Markdown on stdout: kernel-only durations of the unfused variant (its
+    dense kernel and its Tile-COO SpMM kernel, and their sum per launch)
+    beside the fused kernel's, from a --trace-pass-unfused run.  No GPU."""
+    import csv
+    meta = _json_lines(log_path, '{"trace_pass_unfused"')[0]
+    rows = list(csv.DictReader(open(trace_csv)))
+    ks = sorted((r for r in rows if "matmul_kernel" in r["Kernel_Name"]),
+                key=lambda r: int(r["Start_Timestamp"]))[meta["prelude"]:]
+    need = sum(c["dispatches"] for c in meta["trace_pass_unfused"])
+    if len(ks) != need:
+        raise SystemExit(f"{len(ks)} matmul dispatches in the trace, expected {need}")
+
+    def dur(r):
+        return (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+
+    def short(n):
+        return n.replace("void fqk::", "").split("(")[0].strip()
+    res, i = {}, 0
+    for c in meta["trace_pass_unfused"]:
+        chunk = ks[i:i + c["dispatches"]][c["untimed"]:]
+        i += c["dispatches"]
+        if c["per_launch"] == 1:
+            res.setdefault(c["case"], {})["fused"] = (float(np.median([dur(r) for r in chunk])),
+                                                     short(chunk[0]["Kernel_Name"]))
+        else:
+            dense, spmm = chunk[0::2], chunk[1::2]
+            names = ({short(r["Kernel_Name"]) for r in dense}, {short(r["Kernel_Name"]) for r in spmm})
+            if len(names[0]) != 1 or len(names[1]) != 1:
+                raise SystemExit(f"{c['case']}: unfused dispatches do not alternate: {names}")
+            sums = [dur(a) + dur(b) for a, b in zip(dense, spmm)]
+            res[c["case"]]["unfused"] = (float(np.median([dur(r) for r in dense])),
+                                         float(np.median([dur(r) for r in spmm])),
+                                         float(np.median(sums)), names[0].pop(), names[1].pop())
+    L = meta["trace_pass_unfused"][0]["dispatches"] // (1 + TRACE_WARM + TRACE_REPS)
+    out = ["# Unfused variant against the fused kernel: kernel-only durations per matmul "
+           "(rocprofv3 kernel trace), Llama-3-8B decode linears", "",
+           "Commands (repo root, MI355X, ROCm 7.2; `export TMPDIR=/tmp` first), then this "
+           "summary (no GPU):", "",
+           "    rocprofv3 --kernel-trace --output-format csv -d gpurun_out/trace_unf -o run -- "
+           "python3 -u bench.py --trace-pass-unfused > gpurun_out/trace_unf.log",
+           "    python bench.py --trace-unfused-summary gpurun_out/trace_unf/run_kernel_trace.csv "
+           "gpurun_out/trace_unf.log > profiles/unfused_llama3_8b_decode_per_matmul.md", "",
+           f"Each case: a graph of {L} launches of the fused kernel, then one of the unfused "
+           f"variant (its dense kernel writes fp32 partial sums, its SpMM kernel re-reads X and "
+           f"them and adds the outliers), each replayed {TRACE_REPS} times after {TRACE_WARM} "
+           "warm-up replays and the capture's warm-up call (not counted), over the rotated "
+           "weight copies.  `unfused sum` = median over launches of the two kernels' durations "
+           "added; the benchmark's `unfused_us` is the event-timed pair (dispatch gaps "
+           "included).  Kernel sources sha256 (kernels.hip, device.hpp, internal.hpp): "
+           f"`{kernel_source_digest()}`", "",
+           "| matmul | fused us | unfused dense us | unfused SpMM us | unfused sum us | "
+           "unfused sum / fused |", "|---|---|---|---|---|---|"]
+    for case, d in res.items():
+        f = d["fused"][0]
+        ud, us_, usum = d["unfused"][:3]
+        out.append(f"| {case} | {f:.3f} | {ud:.3f} | {us_:.3f} | {usum:.3f} | {usum / f:.2f}x |")
+    kinds = {}
+    for d in res.values():
+        kinds.setdefault("fused", set()).add(d["fused"][1])
+        kinds.setdefault("unfused dense", set()).add(d["unfused"][3])
+        kinds.setdefault("unfused SpMM", set()).add(d["unfused"][4])
+    out += ["", "Kernel instances:", ""]
+    for k, v in kinds.items():
+        out.append(f"- {k}: " + ", ".join(f"`{n}`" for n in sorted(v)))
+    print("\n".join(out))
+
+
 def trace_per_matmul(trace_csv, log_path):
     """Markdown on stdout: rocprofv3 kernel-only durations of a --trace-pass
     run split per (shape, M), and the bf16 GEMM comparator's kernel names.
@@ -1641,6 +1729,13 @@ def main():
                     help="no timing: each matmul's fused graph replayed a fixed number of "
                          "times, then the bf16 GEMM comparator, for a rocprofv3 --kernel-trace "
                          "run split per matmul by --trace-per-matmul")
+    ap.add_argument("--trace-pass-unfused", action="store_true",
+                    help="no timing: each matmul's fused and unfused graphs replayed a fixed "
+                         "number of times, for a rocprofv3 --kernel-trace run summarised by "
+                         "--trace-unfused-summary")
+    ap.add_argument("--trace-unfused-summary", nargs=2, metavar=("KERNEL_TRACE_CSV", "LOG"),
+                    help="no GPU: kernel-only durations of the unfused variant's two kernels "
+                         "beside the fused kernel's, from a --trace-pass-unfused run")
     ap.add_argument("--trace-per-matmul", nargs=2, metavar=("KERNEL_TRACE_CSV", "LOG"),
                     help="no GPU: per-matmul kernel-only durations from a --trace-pass run's "
                          "kernel trace")
@@ -1659,6 +1754,9 @@ def main():
     args = ap.parse_args()
     if args.trace_per_matmul:
         trace_per_matmul(*args.trace_per_matmul)
+        return
+    if args.trace_unfused_summary:
+        trace_unfused_summary(*args.trace_unfused_summary)
         return
     if args.packing_summary:
         packing_summary(*args.packing_summary)
@@ -1809,6 +1907,9 @@ def main():
 
     if args.trace_pass:
         trace_pass(fq, torch, order, launch, R, dev)
+        return
+    if args.trace_pass_unfused:
+        trace_pass_unfused(fq, torch, order, launch, R)
         return
 
     def capture(fn):
